@@ -1,0 +1,262 @@
+/*
+ * Plain fp64 CPU oracle for causal top-k sparse GQA prefill.
+ *
+ * TEST INFRASTRUCTURE ONLY. Only the tests, the smoke check and the
+ * benchmark's CPU-baseline leg load this file's library. The GPU library
+ * shares no code, header, table or helper with it.
+ *
+ * Every function is row-separable: it computes the requested query rows
+ * (or selection blocks) only, so any subset of a long sequence can be
+ * checked exactly. All arithmetic is double precision, written as the
+ * paper's definitions with no blocking, fusion or reordering.
+ *
+ * Notation (0-based): S tokens, Hq query heads, Hkv KV heads, G = Hq/Hkv,
+ * g(h) = floor(h/G), d head dim, d_idx indexer dim, k budget, b selection
+ * block size, block r = queries [r*b, min(r*b+b, S)).
+ * Layouts: q [S,Hq,d], k and v [S,Hkv,d], q_idx and k_idx [S,d_idx].
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_AGG_MAX 0
+#define ORC_AGG_SUM 1
+
+/* Logits of one query row t for one head h against keys 0..t:
+ * l[s] = scale * <q[t,h,:], k[s,g(h),:]>  (Section 3, dense GQA attention). */
+static void logits_row(int Hq, int Hkv, int d, double scale, const double *q,
+                       const double *k, int t, int h, double *l) {
+  int G = Hq / Hkv;
+  int j = h / G;
+  const double *qt = q + ((size_t)t * Hq + h) * d;
+  for (int s = 0; s <= t; ++s) {
+    const double *ks = k + ((size_t)s * Hkv + j) * d;
+    double acc = 0.0;
+    for (int c = 0; c < d; ++c) acc += qt[c] * ks[c];
+    l[s] = scale * acc;
+  }
+}
+
+/* Softmax normaliser: log sum_{s<=t} exp(l[s]), computed with the max shift. */
+static double log_normaliser(const double *l, int n) {
+  double m = -INFINITY;
+  for (int s = 0; s < n; ++s) m = l[s] > m ? l[s] : m;
+  double z = 0.0;
+  for (int s = 0; s < n; ++s) z += exp(l[s] - m);
+  return m + log(z);
+}
+
+/*
+ * Dense causal GQA attention (Section 3, first equation):
+ *   A[t,h,s] = softmax_{s'<=t}(<q_{t,h}, k_{s',g(h)}> * scale)_s
+ *   o[t,h]   = sum_{s<=t} A[t,h,s] v_{s,g(h)}
+ * plus the normaliser lse[t,h] = log sum_{s<=t} exp(l) (Algorithm 1, step 2).
+ * rows[i] is a query position; o is [nrows,Hq,d], lse [nrows,Hq] (either may
+ * be NULL).
+ */
+void orc_dense(int S, int Hq, int Hkv, int d, double scale, const double *q,
+               const double *k, const double *v, int nrows, const int32_t *rows,
+               double *o, double *lse) {
+  (void)S;
+#pragma omp parallel
+  {
+    double *l = (double *)malloc(sizeof(double) * (size_t)S);
+#pragma omp for schedule(dynamic, 1)
+    for (int i = 0; i < nrows; ++i) {
+      int t = rows[i];
+      for (int h = 0; h < Hq; ++h) {
+        int j = h / (Hq / Hkv);
+        logits_row(Hq, Hkv, d, scale, q, k, t, h, l);
+        double lz = log_normaliser(l, t + 1);
+        if (lse) lse[(size_t)i * Hq + h] = lz;
+        if (o) {
+          double *oi = o + ((size_t)i * Hq + h) * d;
+          for (int c = 0; c < d; ++c) oi[c] = 0.0;
+          for (int s = 0; s <= t; ++s) {
+            double a = exp(l[s] - lz);
+            const double *vs = v + ((size_t)s * Hkv + j) * d;
+            for (int c = 0; c < d; ++c) oi[c] += a * vs[c];
+          }
+        }
+      }
+    }
+    free(l);
+  }
+}
+
+/*
+ * Head-averaged attention mass (Section 4.1):
+ *   P_t(s) = (1/Hq) sum_h A[t,h,s],  s <= t.
+ * Following Algorithm 1 steps 2-3: the normaliser of every head is computed
+ * first, then the probabilities are reconstructed and averaged over heads.
+ * P is [nrows,S]; entries s > t are written as 0 and carry no meaning.
+ */
+void orc_mass(int S, int Hq, int Hkv, int d, double scale, const double *q,
+              const double *k, int nrows, const int32_t *rows, double *P) {
+#pragma omp parallel
+  {
+    double *l = (double *)malloc(sizeof(double) * (size_t)S);
+#pragma omp for schedule(dynamic, 1)
+    for (int i = 0; i < nrows; ++i) {
+      int t = rows[i];
+      double *Pi = P + (size_t)i * S;
+      for (int s = 0; s < S; ++s) Pi[s] = 0.0;
+      for (int h = 0; h < Hq; ++h) {
+        logits_row(Hq, Hkv, d, scale, q, k, t, h, l);
+        double lz = log_normaliser(l, t + 1);
+        for (int s = 0; s <= t; ++s) Pi[s] += exp(l[s] - lz);
+      }
+      for (int s = 0; s <= t; ++s) Pi[s] /= (double)Hq;
+    }
+    free(l);
+  }
+}
+
+/*
+ * Head-collapsed indexer score (Section 6.3 equation for z):
+ *   z[t,s] = ReLU(<q_idx[t], k_idx[s]> * scale_idx),  s <= t
+ * with the ReLU skipped when relu == 0. Inputs are the indexer vectors after
+ * key normalisation and RoPE. Z is [nrows,S]; entries s > t are 0.
+ */
+void orc_index_scores(int S, int di, double scale, int relu, const double *qi,
+                      const double *ki, int nrows, const int32_t *rows, double *Z) {
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int i = 0; i < nrows; ++i) {
+    int t = rows[i];
+    double *Zi = Z + (size_t)i * S;
+    const double *qt = qi + (size_t)t * di;
+    for (int s = 0; s < S; ++s) {
+      if (s > t) { Zi[s] = 0.0; continue; }
+      const double *ks = ki + (size_t)s * di;
+      double acc = 0.0;
+      for (int c = 0; c < di; ++c) acc += qt[c] * ks[c];
+      double z = scale * acc;
+      if (relu) z = z > 0.0 ? z : 0.0;
+      Zi[s] = z;
+    }
+  }
+}
+
+/*
+ * Selection-block aggregation (Section 4.2 equation for P_B):
+ *   Y[s] = AGG_{i : trows[i] >= s} X[i][s],  s <= max_i trows[i]
+ * AGG is max (the paper's rule) or sum. X holds one score row per query of
+ * the block ([nt,S]); Y is [S] and is 0 beyond the block's last query.
+ */
+void orc_block_aggregate(int S, int agg, int nt, const int32_t *trows,
+                         const double *X, double *Y) {
+  int tmax = -1;
+  for (int i = 0; i < nt; ++i) tmax = trows[i] > tmax ? trows[i] : tmax;
+  for (int s = 0; s < S; ++s) {
+    if (s > tmax) { Y[s] = 0.0; continue; }
+    int have = 0;
+    double acc = 0.0;
+    for (int i = 0; i < nt; ++i) {
+      if (trows[i] < s) continue;
+      double x = X[(size_t)i * S + s];
+      if (!have) { acc = x; have = 1; }
+      else if (agg == ORC_AGG_MAX) acc = x > acc ? x : acc;
+      else acc += x;
+    }
+    Y[s] = acc;
+  }
+}
+
+typedef struct { double y; int32_t s; } cand_t;
+
+/* Order by score descending, then position ascending. */
+static int cand_cmp(const void *a, const void *b) {
+  const cand_t *x = (const cand_t *)a, *y = (const cand_t *)b;
+  if (x->y > y->y) return -1;
+  if (x->y < y->y) return 1;
+  return (x->s > y->s) - (x->s < y->s);
+}
+
+/*
+ * Top-k support of one score row (Section 4.1 TopK; Algorithm 1 step 4 and
+ * the sentinel padding of step 5). For row i with L = lens[i] valid positions
+ * 0..L-1:
+ *   - if L <= k every valid position is taken;
+ *   - else the Wf = min(W, k) most recent positions are forced, and the
+ *     remaining k - Wf are the first of the other positions in the order
+ *     (score descending, position ascending).
+ * The row of out ([nrows,k]) lists the chosen positions ascending, then -1.
+ */
+void orc_topk(int nrows, const int32_t *lens, const double *Y, int64_t ldy, int k,
+              int W, int32_t *out) {
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int i = 0; i < nrows; ++i) {
+    int L = lens[i];
+    const double *y = Y + (size_t)i * ldy;
+    int32_t *oi = out + (size_t)i * k;
+    for (int c = 0; c < k; ++c) oi[c] = -1;
+    if (L <= k) {
+      for (int s = 0; s < L; ++s) oi[s] = s;
+      continue;
+    }
+    int Wf = W < k ? W : k;
+    int ncand = L - Wf;
+    int kp = k - Wf;
+    cand_t *c = (cand_t *)malloc(sizeof(cand_t) * (size_t)ncand);
+    char *mark = (char *)calloc((size_t)L, 1);
+    for (int s = 0; s < ncand; ++s) { c[s].y = y[s]; c[s].s = s; }
+    qsort(c, (size_t)ncand, sizeof(cand_t), cand_cmp);
+    for (int m = 0; m < kp; ++m) mark[c[m].s] = 1;
+    for (int s = ncand; s < L; ++s) mark[s] = 1;
+    int n = 0;
+    for (int s = 0; s < L; ++s)
+      if (mark[s]) oi[n++] = s;
+    free(c);
+    free(mark);
+  }
+}
+
+/*
+ * Restricted (sparse) attention over a shared support (Section 3, second
+ * equation; Section 4.2 per-query causal mask). Query t belongs to block
+ * r = t / b and uses U = { s in idx[r,:] : 0 <= s <= t, s < S }:
+ *   o[t,h] = sum_{s in U} softmax_U(<q_{t,h}, k_{s,g(h)}> * scale)_s v_{s,g(h)}
+ * with o = 0 when U is empty. idx is [R,kk]; the order of a row and any
+ * sentinel entries do not matter. o is [nrows,Hq,d].
+ */
+void orc_sparse(int S, int Hq, int Hkv, int d, double scale, const double *q,
+                const double *k, const double *v, int b, int kk, const int32_t *idx,
+                int nrows, const int32_t *rows, double *o) {
+  int G = Hq / Hkv;
+#pragma omp parallel
+  {
+    double *l = (double *)malloc(sizeof(double) * (size_t)(kk > 0 ? kk : 1));
+    int32_t *U = (int32_t *)malloc(sizeof(int32_t) * (size_t)(kk > 0 ? kk : 1));
+#pragma omp for schedule(dynamic, 1)
+    for (int i = 0; i < nrows; ++i) {
+      int t = rows[i];
+      int r = t / b;
+      const int32_t *ir = idx + (size_t)r * kk;
+      int n = 0;
+      for (int c = 0; c < kk; ++c)
+        if (ir[c] >= 0 && ir[c] <= t && ir[c] < S) U[n++] = ir[c];
+      for (int h = 0; h < Hq; ++h) {
+        int j = h / G;
+        double *oi = o + ((size_t)i * Hq + h) * d;
+        for (int c = 0; c < d; ++c) oi[c] = 0.0;
+        if (n == 0) continue;
+        const double *qt = q + ((size_t)t * Hq + h) * d;
+        for (int u = 0; u < n; ++u) {
+          const double *ks = k + ((size_t)U[u] * Hkv + j) * d;
+          double acc = 0.0;
+          for (int c = 0; c < d; ++c) acc += qt[c] * ks[c];
+          l[u] = scale * acc;
+        }
+        double lz = log_normaliser(l, n);
+        for (int u = 0; u < n; ++u) {
+          double a = exp(l[u] - lz);
+          const double *vs = v + ((size_t)U[u] * Hkv + j) * d;
+          for (int c = 0; c < d; ++c) oi[c] += a * vs[c];
+        }
+      }
+    }
+    free(l);
+    free(U);
+  }
+}

@@ -1,0 +1,131 @@
+"""Seeded synthetic inputs: Q/K/V, head-collapsed indexer vectors, planted needles.
+
+Recipe (one numpy PCG64 stream per call, fixed draw order):
+
+1. Q [S,Hq,d], K [S,Hkv,d], V [S,Hkv,d] ~ N(0,1)/sqrt(d) (``peaked=True``
+   drops the 1/sqrt(d), giving logits of unit spread instead of ~1/d).
+2. q_idx, k_idx [S,d_idx] ~ N(0,1) (the indexer's post-normalisation,
+   post-RoPE vectors of Section 6.3; the projection itself is not modelled).
+3. Needles: n positions p_i (uniform without replacement, or stratified
+   p_i = floor((i+u_i)*S/n)), each with a probe query r_i ~ U[p_i, S) and a
+   probe head h_i ~ U[0, Hq). K[p_i, every KV head] = 3 * Q[r_i,h_i]/|Q[r_i,h_i]|.
+   When an indexer is present and not ``untrained``, also
+   k_idx[p_i] = 3*sqrt(d_idx) * q_idx[r_i]/|q_idx[r_i]|.
+4. Everything is drawn in fp32 and rounded once to the storage dtype
+   (bf16 by round-to-nearest-even through torch).
+
+Needle retrieval mirrors the needle-in-a-haystack task family the paper
+evaluates on (Section 5.1); no benchmark item is reproduced.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional
+
+import numpy as np
+import torch
+
+_TORCH_DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+@dataclasses.dataclass
+class Inputs:
+    q: torch.Tensor
+    k: torch.Tensor
+    v: torch.Tensor
+    q_idx: Optional[torch.Tensor]
+    k_idx: Optional[torch.Tensor]
+    needle_pos: np.ndarray    # [n] int64
+    probe_query: np.ndarray   # [n] int64
+    probe_head: np.ndarray    # [n] int64
+
+    def to(self, device) -> "Inputs":
+        mv = lambda t: None if t is None else t.to(device)
+        return dataclasses.replace(self, q=mv(self.q), k=mv(self.k), v=mv(self.v),
+                                   q_idx=mv(self.q_idx), k_idx=mv(self.k_idx))
+
+
+def _rng(seed: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+def make_inputs(seq_len: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                index_dim: int = 0, dtype: str = "bf16", needles: int = 0,
+                stratified: bool = False, seed: int = 0, peaked: bool = False,
+                untrained: bool = False) -> Inputs:
+    S, Hq, Hkv, d, di = seq_len, num_q_heads, num_kv_heads, head_dim, index_dim
+    rng = _rng(seed)
+    sd = 1.0 if peaked else 1.0 / np.sqrt(d)
+    q = rng.standard_normal((S, Hq, d), dtype=np.float32) * np.float32(sd)
+    k = rng.standard_normal((S, Hkv, d), dtype=np.float32) * np.float32(sd)
+    v = rng.standard_normal((S, Hkv, d), dtype=np.float32) * np.float32(1.0 / np.sqrt(d))
+    qi = ki = None
+    if di > 0:
+        qi = rng.standard_normal((S, di), dtype=np.float32)
+        ki = rng.standard_normal((S, di), dtype=np.float32)
+    n = min(needles, S)
+    if n > 0:
+        if stratified:
+            u = rng.random(n)
+            pos = np.floor((np.arange(n) + u) * S / n).astype(np.int64)
+            pos = np.minimum(pos, S - 1)
+        else:
+            pos = np.sort(rng.choice(S, size=n, replace=False)).astype(np.int64)
+        probe_q = (pos + np.floor(rng.random(n) * (S - pos))).astype(np.int64)
+        probe_q = np.minimum(probe_q, S - 1)
+        probe_h = rng.integers(0, Hq, size=n).astype(np.int64)
+        for p, r, h in zip(pos, probe_q, probe_h):
+            u = q[r, h] / np.linalg.norm(q[r, h])
+            k[p, :, :] = 3.0 * u[None, :]
+            if di > 0 and not untrained:
+                qn = qi[r] / np.linalg.norm(qi[r])
+                ki[p] = 3.0 * np.sqrt(di) * qn
+    else:
+        pos = probe_q = probe_h = np.zeros(0, dtype=np.int64)
+    td = _TORCH_DTYPES[dtype]
+    cv = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(td)
+    return Inputs(q=cv(q), k=cv(k), v=cv(v), q_idx=cv(qi), k_idx=cv(ki),
+                  needle_pos=pos, probe_query=probe_q, probe_head=probe_h)
+
+
+def make_scores(rows: int, seq_len: int, seed: int = 0, kind: str = "gauss") -> torch.Tensor:
+    """Score rows [rows, seq_len] fp32 for exercising top-k on its own.
+
+    kind: "gauss" (distinct values), "relu" (about half exact zeros, with some
+    negative zeros), "coarse" (values on a grid of 16 levels, so many exact
+    ties), "const" (every entry equal).
+    """
+    rng = _rng(seed)
+    x = rng.standard_normal((rows, seq_len), dtype=np.float32)
+    if kind == "relu":
+        x = np.maximum(x, np.float32(0.0))
+        neg0 = rng.random((rows, seq_len)) < 0.1
+        x[neg0 & (x == 0)] = np.float32(-0.0)
+    elif kind == "coarse":
+        x = np.round(x * 4.0).astype(np.float32) / np.float32(4.0)
+    elif kind == "const":
+        x[:] = np.float32(0.5)
+    elif kind != "gauss":
+        raise ValueError(kind)
+    return torch.from_numpy(np.ascontiguousarray(x))
+
+
+def make_support(seq_len: int, block_q: int, topk: int, seed: int = 0,
+                 shuffle: bool = False) -> torch.Tensor:
+    """A random support table [R, topk] int32 for exercising sparse attention alone.
+
+    Row r draws min(topk, t1_r+1) distinct positions from [0, t1_r], where t1_r
+    is the last query of selection block r, stores them ascending (or shuffled)
+    and pads with -1.
+    """
+    rng = _rng(seed)
+    R = (seq_len + block_q - 1) // block_q
+    out = np.full((R, topk), -1, dtype=np.int32)
+    for r in range(R):
+        t1 = min(r * block_q + block_q, seq_len) - 1
+        m = min(topk, t1 + 1)
+        sel = np.sort(rng.choice(t1 + 1, size=m, replace=False))
+        if shuffle:
+            sel = rng.permutation(sel)
+        out[r, :m] = sel
+    return torch.from_numpy(out)
