@@ -1,0 +1,179 @@
+/*
+ * sparse_prefill.h — C ABI of the MI355X (gfx950) causal top-k sparse GQA
+ * prefill library.
+ *
+ * The library computes, for one grouped-query-attention layer, the sparse
+ * prefill path of "How Much Dense Attention is Necessary? Oracle-Guided
+ * Sparse Prefill for Full/GQA Layers in Hybrid Long-Context Models":
+ *
+ *   indexer mode (Algorithm 2, steps 4-5):
+ *     sp_indexer_scores -> sp_topk_select -> sp_sparse_gqa_attn
+ *   oracle mode (Algorithm 1, steps 2-5):
+ *     sp_dense_attn (normalisers) -> sp_oracle_support -> sp_topk_select
+ *     -> sp_sparse_gqa_attn
+ *   dense baseline (Section 3):
+ *     sp_dense_attn
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Indices are 0-based. S = seq_len, Hq query heads, Hkv KV heads,
+ * G = Hq/Hkv, query head h reads KV head g(h) = floor(h/G) (contiguous
+ * groups), d = head_dim, d_idx = index_dim, k = topk, b = block_q (the
+ * selection block size b_sel), R = ceil(S/b) selection blocks; block r
+ * holds queries t0_r = r*b ... t1_r = min(r*b+b, S)-1.
+ *
+ * Layouts (all contiguous, row-major, element type = problem dtype unless
+ * stated):
+ *   q, o          [S, Hq,  d]
+ *   k, v          [S, Hkv, d]
+ *   q_idx, k_idx  [S, d_idx]
+ *   lse           [S, Hq]  float32
+ *   scores, mass  [R, S]   float32; row r is valid for columns s <= t1_r
+ *                          only: later columns are never written nor read
+ *   idx           [R, k]   int32; ascending positions, then -1 sentinels;
+ *                          one row serves every query of block r and every
+ *                          KV head
+ *
+ * Memory and ownership: every pointer is a DEVICE pointer allocated and
+ * owned by the caller, 16-byte aligned, and inputs never alias outputs.
+ * The library allocates nothing and keeps no mutable global state apart
+ * from a per-device cache of the device architecture.
+ *
+ * Execution: each call validates its arguments on the host before any HIP
+ * call (so validation needs no GPU), then enqueues its kernels on `stream`
+ * and returns without synchronising. Faults inside a kernel surface at the
+ * caller's next synchronisation.
+ *
+ * Errors: each entry point returns SP_OK or a negative sp_status; on error
+ * nothing has been enqueued.
+ */
+#ifndef SPARSE_PREFILL_H_
+#define SPARSE_PREFILL_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SP_VERSION 10000 /* 1.0.0 */
+
+typedef enum sp_status {
+  SP_OK = 0,
+  SP_ERR_NULL = -1,        /* a required pointer is NULL */
+  SP_ERR_SHAPE = -2,       /* inconsistent sizes (e.g. Hq % Hkv != 0, k < 1) */
+  SP_ERR_UNSUPPORTED = -3, /* valid but not built: head_dim, dtype, causal=0 */
+  SP_ERR_WORKSPACE = -4,   /* workspace smaller than sp_workspace_bytes */
+  SP_ERR_ALIGN = -5,       /* a pointer is not 16-byte aligned */
+  SP_ERR_NO_DEVICE = -6,   /* no HIP device is usable */
+  SP_ERR_ARCH = -7,        /* current device is not gfx950 */
+  SP_ERR_HIP = -8          /* a HIP launch failed */
+} sp_status;
+
+enum { SP_DTYPE_F32 = 0, SP_DTYPE_BF16 = 1 };
+enum { SP_AGG_MAX = 0, SP_AGG_SUM = 1 };
+enum { SP_OP_DENSE = 0, SP_OP_ORACLE = 1, SP_OP_INDEXER = 2, SP_OP_TOPK = 3,
+       SP_OP_SPARSE = 4 };
+
+/*
+ * One GQA layer's sparse-prefill problem (Section 3: S, Hq, Hkv, d_h, the
+ * map g; Section 3 support granularity: b_sel; Section 3 restricted
+ * attention: |S_t| <= k; Section 6.3: d_idx).
+ */
+typedef struct sp_problem {
+  int32_t seq_len;      /* S >= 1 */
+  int32_t num_q_heads;  /* Hq >= 1, a multiple of num_kv_heads */
+  int32_t num_kv_heads; /* Hkv >= 1 */
+  int32_t head_dim;     /* d: 64 or 128 */
+  int32_t index_dim;    /* d_idx: 64, 128 or 256 (indexer calls only) */
+  int32_t topk;         /* k >= 1; k >= t1_r+1 keeps every causal key */
+  int32_t block_q;      /* b >= 1; 1 = per-query support */
+  int32_t causal;       /* must be 1: the paper's attention is causal */
+  int32_t local_window; /* W in [0, k]: the W most recent positions of each
+                           block are always selected, counted inside k */
+  int32_t agg;          /* SP_AGG_MAX (Section 4.2) or SP_AGG_SUM */
+  int32_t relu;         /* 1: ReLU on indexer scores (Section 6.3); 0: raw */
+  int32_t dtype;        /* SP_DTYPE_F32 or SP_DTYPE_BF16 for q,k,v,o,q_idx,k_idx */
+  float attn_scale;     /* 0 => 1/sqrt(d) (Section 3) */
+  float index_scale;    /* 0 => 1/sqrt(d_idx) (Section 6.3) */
+} sp_problem;
+
+/*
+ * Dense causal GQA attention (Section 3, first equation; Algorithm 1 step 2).
+ *   o[t,h]   = sum_{s<=t} softmax_{s'<=t}(attn_scale * <q[t,h], k[s',g(h)]>)_s v[s,g(h)]
+ *   lse[t,h] = log sum_{s<=t} exp(attn_scale * <q[t,h], k[s,g(h)]>)
+ * o may be NULL when lse is given: only the softmax normalisers are
+ * computed (what the oracle needs). lse may be NULL. Both NULL is
+ * SP_ERR_NULL. Fields used: seq_len, heads, head_dim, causal, dtype,
+ * attn_scale.
+ */
+int sp_dense_attn(const sp_problem *p, const void *q, const void *k, const void *v,
+                  void *o, float *lse, hipStream_t stream);
+
+/*
+ * Attention-mass oracle scores (Section 4.1 head-averaged mass; Section 4.2
+ * block max; Algorithm 1 step 3):
+ *   P_t(s)    = (1/Hq) sum_h exp(attn_scale * <q[t,h], k[s,g(h)]> - lse[t,h]),  s <= t
+ *   mass[r,s] = AGG_{t in block r, t >= s} P_t(s),  s <= t1_r
+ * lse must come from sp_dense_attn on the same q, k and problem. AGG is
+ * `agg` (the paper's rule is max); with block_q = 1 mass[t,s] = P_t(s).
+ */
+int sp_oracle_support(const sp_problem *p, const void *q, const void *k, const float *lse,
+                      float *mass, hipStream_t stream);
+
+/*
+ * Head-collapsed indexer scores (Section 6.3 equation for z; Algorithm 2
+ * step 4):
+ *   z[t,s]      = ReLU(index_scale * <q_idx[t], k_idx[s]>),  s <= t  (no ReLU if relu=0)
+ *   scores[r,s] = AGG_{t in block r, t >= s} z[t,s],  s <= t1_r
+ * q_idx/k_idx are the indexer vectors after key normalisation, RoPE and
+ * any query scale (Algorithm 2 step 3).
+ */
+int sp_indexer_scores(const sp_problem *p, const void *q_idx, const void *k_idx,
+                      float *scores, hipStream_t stream);
+
+/*
+ * Top-k support selection (Section 4.1 TopK; Section 4.2; Algorithm 1
+ * steps 4-5; Algorithm 2 step 5). For block r with L = t1_r+1 causal
+ * positions:
+ *   L <= k : idx[r] = 0..L-1, then -1;
+ *   L >  k : the Wf = min(local_window, k) positions t1_r-Wf+1..t1_r are
+ *            forced; the other k-Wf are the first positions of 0..L-Wf-1
+ *            in the order (score descending, position ascending), with
+ *            -0.0 treated as +0.0.
+ * Each row is written ascending. NaN scores give an unspecified (but
+ * in-bounds) selection. workspace may be NULL when sp_workspace_bytes
+ * reports 0 for SP_OP_TOPK (it does in this version).
+ */
+int sp_topk_select(const sp_problem *p, const float *scores, int32_t *idx, void *workspace,
+                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Sparse GQA attention over the shared supports (Section 3, second
+ * equation; Section 4.2 per-query causal mask; Algorithm 1 step 5).
+ * Query t of block r = t/b, head h, uses U = { s in idx[r,:] : 0 <= s <= t }:
+ *   o[t,h] = sum_{s in U} softmax_U(attn_scale * <q[t,h], k[s,g(h)]>)_s v[s,g(h)]
+ * and o[t,h] = 0 when U is empty. Entries < 0 or >= S are skipped (they are
+ * sentinels); positions within a row must be distinct. The order of a row
+ * does not change the result beyond rounding.
+ */
+int sp_sparse_gqa_attn(const sp_problem *p, const void *q, const void *k, const void *v,
+                       const int32_t *idx, void *o, hipStream_t stream);
+
+/* Device workspace (bytes) an operation needs for problem p; 0 = none. */
+int sp_workspace_bytes(const sp_problem *p, int op, size_t *bytes);
+
+/* Static, human-readable text for a status code. */
+const char *sp_status_string(int status);
+
+/* SP_VERSION of the built library. */
+int sp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARSE_PREFILL_H_ */

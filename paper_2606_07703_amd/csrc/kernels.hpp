@@ -1,0 +1,35 @@
+// Internal launch interface between the C ABI (api.cpp) and the kernels.
+// Every launcher assumes its problem has been validated by the host layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sparse_prefill.h"
+
+namespace sp {
+
+// A validated problem with defaults resolved.
+struct Prob {
+  int S, Hq, Hkv, G, d, di, k, b, R, W, agg, relu, dtype;
+  float scale;   // attention logit scale
+  float iscale;  // indexer score scale
+};
+
+// Dense (idx == nullptr) or sparse (idx != nullptr) attention, one wave per
+// (query, head chunk). o and/or lse may be null.
+hipError_t launch_attn_rowwise(const Prob &p, const void *q, const void *k, const void *v,
+                               const int32_t *idx, void *o, float *lse, hipStream_t st);
+
+// Head-averaged mass with block aggregation.
+hipError_t launch_mass_rowwise(const Prob &p, const void *q, const void *k, const float *lse,
+                               float *mass, hipStream_t st);
+
+// Indexer scores with block aggregation.
+hipError_t launch_indexer_rowwise(const Prob &p, const void *qi, const void *ki, float *scores,
+                                  hipStream_t st);
+
+// Row-wise top-k selection.
+hipError_t launch_topk(const Prob &p, const float *scores, int32_t *idx, hipStream_t st);
+
+}  // namespace sp

@@ -1,0 +1,214 @@
+"""GPU parity, one entry point at a time, against the fp64 oracle.
+
+Inputs come from the seeded generator only (supports and score rows too), so
+each kernel is checked in isolation from the others. Sizes span several
+tiles and end in ragged tails.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_07703_amd import binding as B
+from synth import make_inputs, make_scores, make_support
+
+from helpers import check_rows_ascending, cuda, f64, max_err, say, tol_for
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load()
+
+
+def _inp(S, Hq, Hkv, d, di=0, dtype="bf16", seed=0, peaked=False, needles=0):
+    return make_inputs(S, Hq, Hkv, d, index_dim=di, dtype=dtype, needles=needles, seed=seed,
+                       peaked=peaked)
+
+
+# ------------------------------------------------------------ sparse attention
+SPARSE_CASES = [
+    # S, Hq, Hkv, d, dtype, b, k
+    (1, 4, 2, 64, "f32", 1, 1),
+    (300, 4, 2, 64, "f32", 1, 37),
+    (300, 6, 2, 64, "f32", 16, 64),
+    (300, 4, 4, 128, "f32", 64, 100),
+    (257, 8, 2, 128, "bf16", 1, 64),
+    (257, 8, 2, 128, "bf16", 64, 128),
+    (300, 16, 4, 128, "bf16", 16, 200),
+    (300, 2, 1, 64, "bf16", 7, 5),
+    (200, 8, 8, 128, "bf16", 1, 250),
+    (520, 32, 8, 128, "bf16", 64, 256),
+    (520, 32, 8, 128, "bf16", 128, 96),
+]
+
+
+@pytest.mark.parametrize("case", SPARSE_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_sparse_attention(case):
+    S, Hq, Hkv, d, dtype, b, k = case
+    say(f"sparse {case}")
+    inp = _inp(S, Hq, Hkv, d, dtype=dtype, seed=S + k, peaked=(dtype == "f32"))
+    idx = make_support(S, b, k, seed=b)
+    p = B.Problem(S, Hq, Hkv, d, topk=k, block_q=b, dtype=dtype)
+    o = torch.empty(S, Hq, d, dtype=inp.q.dtype, device="cuda")
+    B.sp_sparse_gqa_attn(p, cuda(inp.q), cuda(inp.k), cuda(inp.v), cuda(idx), o)
+    torch.cuda.synchronize()
+    ref = oracle.sparse(inp.q, inp.k, inp.v, idx, b)
+    err = max_err(f64(o), ref)
+    say(f"  max abs err {err:.3e} (max |ref| {np.abs(ref).max():.3e})")
+    assert err <= tol_for(dtype)
+
+
+def test_sparse_attention_order_and_sentinels():
+    S, Hq, Hkv, d, b, k = 300, 8, 2, 128, 16, 64
+    say("sparse shuffled support")
+    inp = _inp(S, Hq, Hkv, d, dtype="f32", seed=5, peaked=True)
+    idx = make_support(S, b, k, seed=1)
+    rng = np.random.default_rng(0)
+    shuf = torch.from_numpy(np.stack([rng.permutation(r) for r in idx.numpy()]))
+    pad = torch.cat([shuf, torch.full((shuf.shape[0], 9), -1, dtype=torch.int32),
+                     torch.full((shuf.shape[0], 3), S + 50, dtype=torch.int32)], dim=1)
+    outs = []
+    for table in (idx, pad):
+        p = B.Problem(S, Hq, Hkv, d, topk=table.shape[1], block_q=b, dtype="f32")
+        o = torch.empty(S, Hq, d, device="cuda")
+        B.sp_sparse_gqa_attn(p, cuda(inp.q), cuda(inp.k), cuda(inp.v), cuda(table.contiguous()),
+                             o)
+        outs.append(f64(o))
+    assert max_err(outs[0], outs[1]) < 1e-6
+
+
+# ----------------------------------------------------------------------- dense
+DENSE_CASES = [
+    (1, 4, 2, 64, "f32"),
+    (77, 4, 2, 64, "f32"),
+    (300, 6, 3, 128, "f32"),
+    (300, 8, 2, 128, "bf16"),
+    (515, 32, 8, 128, "bf16"),
+    (260, 4, 4, 64, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", DENSE_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_dense_attention(case):
+    S, Hq, Hkv, d, dtype = case
+    say(f"dense {case}")
+    inp = _inp(S, Hq, Hkv, d, dtype=dtype, seed=S, peaked=(dtype == "f32"), needles=min(S, 4))
+    p = B.Problem(S, Hq, Hkv, d, dtype=dtype)
+    o = torch.empty(S, Hq, d, dtype=inp.q.dtype, device="cuda")
+    lse = torch.empty(S, Hq, device="cuda")
+    lse2 = torch.empty(S, Hq, device="cuda")
+    q, k, v = cuda(inp.q), cuda(inp.k), cuda(inp.v)
+    B.sp_dense_attn(p, q, k, v, o, lse)
+    B.sp_dense_attn(p, q, k, v, None, lse2)
+    torch.cuda.synchronize()
+    ref_o, ref_lse = oracle.dense(inp.q, inp.k, inp.v)
+    eo, el = max_err(f64(o), ref_o), max_err(f64(lse), ref_lse)
+    say(f"  o err {eo:.3e}  lse err {el:.3e}")
+    assert eo <= tol_for(dtype)
+    assert el <= (1e-5 if dtype == "f32" else 1e-4)
+    assert torch.equal(lse, lse2)
+
+
+# ----------------------------------------------------------------------- top-k
+TOPK_CASES = [
+    # R-defining (S, b), k, W, kind
+    (300, 1, 37, 0, "gauss"),
+    (300, 1, 37, 5, "relu"),
+    (300, 7, 64, 0, "coarse"),
+    (300, 64, 100, 16, "gauss"),
+    (300, 64, 100, 100, "gauss"),
+    (300, 3, 1, 0, "coarse"),
+    (300, 3, 1, 1, "relu"),
+    (300, 1, 299, 0, "const"),
+    (5000, 64, 512, 0, "relu"),
+    (9000, 128, 2048, 128, "gauss"),
+    (9000, 128, 700, 0, "coarse"),
+]
+
+
+@pytest.mark.parametrize("case", TOPK_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_topk(case):
+    S, b, k, W, kind = case
+    say(f"topk {case}")
+    R = (S + b - 1) // b
+    scores = make_scores(R, S, seed=S + k, kind=kind)
+    p = B.Problem(S, 1, 1, 64, topk=k, block_q=b, local_window=W, dtype="f32")
+    idx = torch.empty(R, k, dtype=torch.int32, device="cuda")
+    B.sp_topk_select(p, cuda(scores), idx)
+    torch.cuda.synchronize()
+    lens = np.array([min(r * b + b, S) for r in range(R)])
+    ref = oracle.topk(scores.numpy().astype(np.float64), lens, k, W)
+    got = idx.cpu().numpy()
+    check_rows_ascending(got, lens, k)
+    assert np.array_equal(got, ref)   # same fp32 values: selection must be bit-exact
+
+
+# --------------------------------------------------------------- indexer scores
+INDEXER_CASES = [
+    # S, d_idx, b, agg, relu, dtype
+    (300, 64, 1, "max", 1, "bf16"),
+    (300, 128, 16, "max", 1, "bf16"),
+    (300, 128, 64, "sum", 1, "bf16"),
+    (300, 256, 64, "max", 0, "bf16"),
+    (300, 64, 7, "sum", 0, "f32"),
+    (1000, 128, 128, "max", 1, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", INDEXER_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_indexer_scores(case):
+    S, di, b, agg, relu, dtype = case
+    say(f"indexer {case}")
+    inp = _inp(S, 1, 1, 64, di=di, dtype=dtype, seed=di + b, needles=8)
+    p = B.Problem(S, 1, 1, 64, index_dim=di, topk=8, block_q=b, agg=agg, relu=relu, dtype=dtype)
+    R = p.num_blocks
+    sc = torch.full((R, S), float("nan"), device="cuda")
+    B.sp_indexer_scores(p, cuda(inp.q_idx), cuda(inp.k_idx), sc)
+    torch.cuda.synchronize()
+    ref = oracle.support_scores("indexer", range(R), b, q_idx=inp.q_idx, k_idx=inp.k_idx,
+                                agg=agg, relu=bool(relu))
+    got = sc.cpu().numpy().astype(np.float64)
+    scale = np.abs(ref).max()
+    for r in range(R):
+        L = min(r * b + b, S)
+        e = max_err(got[r, :L], ref[r, :L])
+        assert e <= 2e-6 * scale * (b if agg == "sum" else 1), (r, e, scale)
+        assert np.all(np.isnan(got[r, L:]))   # invalid tail untouched
+
+
+# ------------------------------------------------------------------ oracle mass
+MASS_CASES = [
+    # S, Hq, Hkv, d, b, agg, dtype
+    (200, 4, 2, 64, 1, "max", "f32"),
+    (200, 4, 2, 64, 8, "max", "f32"),
+    (300, 8, 2, 128, 64, "max", "bf16"),
+    (300, 8, 2, 128, 16, "sum", "bf16"),
+    (260, 32, 8, 128, 1, "max", "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", MASS_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_oracle_mass(case):
+    S, Hq, Hkv, d, b, agg, dtype = case
+    say(f"mass {case}")
+    inp = _inp(S, Hq, Hkv, d, dtype=dtype, seed=S + b, peaked=True, needles=4)
+    p = B.Problem(S, Hq, Hkv, d, topk=8, block_q=b, agg=agg, dtype=dtype)
+    q, k, v = cuda(inp.q), cuda(inp.k), cuda(inp.v)
+    lse = torch.empty(S, Hq, device="cuda")
+    B.sp_dense_attn(p, q, k, v, None, lse)
+    R = p.num_blocks
+    mass = torch.full((R, S), float("nan"), device="cuda")
+    B.sp_oracle_support(p, q, k, lse, mass)
+    torch.cuda.synchronize()
+    ref = oracle.support_scores("oracle", range(R), b, q=inp.q, k=inp.k, agg=agg)
+    got = mass.cpu().numpy().astype(np.float64)
+    for r in range(R):
+        L = min(r * b + b, S)
+        e = max_err(got[r, :L], ref[r, :L])
+        scale = np.abs(ref[r, :L]).max()
+        assert e <= 1e-4 * scale, (r, e, scale)
+        assert np.all(np.isnan(got[r, L:]))

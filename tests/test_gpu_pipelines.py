@@ -1,0 +1,241 @@
+"""GPU parity of whole call sequences against the fp64 oracle.
+
+Small problems are compared on every row. The named workloads (up to the
+102,400-token stress shape) run at full size, exactly as the benchmark
+launches them, and are compared on sampled selection blocks and query rows
+that the oracle computes one by one: the first and last blocks, the blocks
+of needle probes, and seeded random blocks.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_07703_amd import binding as B
+from paper_2606_07703_amd import pipeline as PL
+from synth import get_workload, make_inputs
+
+from helpers import (check_rows_ascending, compare_support, cuda, f64, max_err, say,
+                     tol_for)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load()
+
+
+def _lens(S, b, units):
+    return np.array([min(r * b + b, S) for r in units])
+
+
+def check_pipeline(p: B.Problem, inp, buf, mode: str, units, rows_per_unit=None,
+                   tol=None, want_needles=True):
+    """Compare supports of `units` and outputs of their queries with the oracle."""
+    S, b, k, W = p.seq_len, p.block_q, p.topk, p.local_window
+    units = sorted(set(int(u) for u in units))
+    if mode == "indexer":
+        Y = oracle.support_scores("indexer", units, b, q_idx=inp.q_idx, k_idx=inp.k_idx,
+                                  agg=p.agg, relu=p.relu)
+    else:
+        Y = oracle.support_scores("oracle", units, b, q=inp.q, k=inp.k, agg=p.agg)
+    ref_idx = oracle.select(Y, units, b, S, k, W)
+    gpu_idx_all = buf.idx.cpu().numpy()
+    gpu_idx = gpu_idx_all[units]
+    lens = _lens(S, b, units)
+    check_rows_ascending(gpu_idx, lens, k)
+    kinds = [compare_support(gpu_idx[i], ref_idx[i], Y[i], int(lens[i]), k, W)
+             for i in range(len(units))]
+    say(f"  supports: {kinds.count('exact')} exact, {kinds.count('tolerant')} tolerant")
+    # outputs on the sampled units' queries, where the selected sets agree
+    same = {u: np.array_equal(gpu_idx[i], ref_idx[i]) for i, u in enumerate(units)}
+    rows = []
+    for u in units:
+        if not same[u]:
+            continue
+        q_rows = list(range(u * b, min(u * b + b, S)))
+        if rows_per_unit and len(q_rows) > rows_per_unit:
+            q_rows = q_rows[:: max(1, len(q_rows) // rows_per_unit)][:rows_per_unit] + [q_rows[-1]]
+        rows += q_rows
+    table = np.full((p.num_blocks, k), -1, dtype=np.int32)
+    for i, u in enumerate(units):
+        table[u] = ref_idx[i]
+    if rows:
+        ref_o = oracle.sparse(inp.q, inp.k, inp.v, table, b, rows=rows)
+        got_o = f64(buf.o[torch.as_tensor(rows, device=buf.o.device)])
+        err = max_err(got_o, ref_o)
+        say(f"  outputs: {len(rows)} rows, max abs err {err:.3e}, max|ref| "
+            f"{np.abs(ref_o).max():.3e}")
+        assert err <= (tol if tol is not None else tol_for(p.dtype))
+    if want_needles and mode == "indexer":
+        sup = {u: set(gpu_idx_all[u].tolist()) for u in range(p.num_blocks)}
+        hit = [int(pos) in sup[int(r) // b] for pos, r in zip(inp.needle_pos, inp.probe_query)]
+        say(f"  needles retrieved: {sum(hit)}/{len(hit)}")
+        assert all(hit)
+    return kinds
+
+
+# ------------------------------------------------------------------- small, all rows
+@pytest.mark.parametrize("b,W,agg", [(1, 0, "max"), (1, 8, "max"), (32, 0, "max"),
+                                     (32, 16, "sum"), (64, 64, "max")])
+def test_indexer_pipeline_small(b, W, agg):
+    S, Hq, Hkv, d, di, k = 700, 8, 2, 128, 64, 64
+    say(f"indexer pipeline S={S} b={b} W={W} agg={agg}")
+    inp = make_inputs(S, Hq, Hkv, d, index_dim=di, dtype="bf16", needles=16, seed=b + W)
+    p = B.Problem(S, Hq, Hkv, d, index_dim=di, topk=k, block_q=b, local_window=W, agg=agg)
+    buf = PL.indexer_prefill(p, cuda(inp.q), cuda(inp.k), cuda(inp.v), cuda(inp.q_idx),
+                             cuda(inp.k_idx))
+    torch.cuda.synchronize()
+    # W = k leaves nothing to select: the support is the forced window alone
+    check_pipeline(p, inp, buf, "indexer", range(p.num_blocks), want_needles=W < k // 2)
+
+
+def test_oracle_pipeline_tiny_workload():
+    w = get_workload("oracle_tiny_512")
+    say(f"oracle pipeline {w.name}")
+    inp = make_inputs(w.seq_len, w.num_q_heads, w.num_kv_heads, w.head_dim, dtype=w.dtype,
+                      needles=w.needles, seed=w.seed)
+    p = B.Problem(w.seq_len, w.num_q_heads, w.num_kv_heads, w.head_dim, topk=w.topk,
+                  block_q=1, dtype=w.dtype)
+    buf = PL.oracle_prefill(p, cuda(inp.q), cuda(inp.k), cuda(inp.v))
+    torch.cuda.synchronize()
+    assert buf.o.shape == (512, 4, 64) and buf.idx.shape == (512, 64)
+    check_pipeline(p, inp, buf, "oracle", range(p.num_blocks))
+    sup = buf.idx.cpu().numpy()
+    hit = [int(pos) in set(sup[int(r)].tolist()) for pos, r in zip(inp.needle_pos,
+                                                                   inp.probe_query)]
+    say(f"  needles retrieved: {sum(hit)}/{len(hit)}")
+    assert all(hit)
+
+
+def test_oracle_pipeline_peaked_block():
+    S, Hq, Hkv, d, k, b = 400, 8, 2, 128, 48, 16
+    say("oracle pipeline peaked bf16 b=16")
+    inp = make_inputs(S, Hq, Hkv, d, dtype="bf16", needles=8, seed=7, peaked=True)
+    p = B.Problem(S, Hq, Hkv, d, topk=k, block_q=b, dtype="bf16")
+    buf = PL.oracle_prefill(p, cuda(inp.q), cuda(inp.k), cuda(inp.v))
+    torch.cuda.synchronize()
+    kinds = check_pipeline(p, inp, buf, "oracle", range(p.num_blocks))
+    assert kinds.count("exact") >= len(kinds) // 2
+
+
+def test_sparse_on_oracle_supports():
+    """K5 numerics on the oracle's own supports (no dependence on GPU selection)."""
+    S, Hq, Hkv, d, k, b = 600, 16, 4, 128, 100, 1
+    say("sparse attention on oracle supports")
+    inp = make_inputs(S, Hq, Hkv, d, index_dim=64, dtype="bf16", needles=8, seed=3)
+    units = range((S + b - 1) // b)
+    Y = oracle.support_scores("indexer", units, b, q_idx=inp.q_idx, k_idx=inp.k_idx)
+    idx = torch.from_numpy(oracle.select(Y, units, b, S, k))
+    p = B.Problem(S, Hq, Hkv, d, index_dim=64, topk=k, block_q=b)
+    o = torch.empty(S, Hq, d, dtype=torch.bfloat16, device="cuda")
+    B.sp_sparse_gqa_attn(p, cuda(inp.q), cuda(inp.k), cuda(inp.v), cuda(idx), o)
+    torch.cuda.synchronize()
+    ref = oracle.sparse(inp.q, inp.k, inp.v, idx, b)
+    assert max_err(f64(o), ref) <= 2e-2
+
+
+def test_full_budget_matches_dense():
+    S, Hq, Hkv, d = 300, 8, 2, 128
+    say("full budget equals dense")
+    inp = make_inputs(S, Hq, Hkv, d, index_dim=64, dtype="bf16", seed=9)
+    p = B.Problem(S, Hq, Hkv, d, index_dim=64, topk=S, block_q=16)
+    buf = PL.indexer_prefill(p, cuda(inp.q), cuda(inp.k), cuda(inp.v), cuda(inp.q_idx),
+                             cuda(inp.k_idx))
+    od = PL.dense_prefill(p, cuda(inp.q), cuda(inp.k), cuda(inp.v))
+    torch.cuda.synchronize()
+    lens = _lens(S, 16, range(p.num_blocks))
+    check_rows_ascending(buf.idx.cpu().numpy(), lens, S)
+    assert max_err(f64(buf.o), f64(od)) <= 1e-2
+
+
+def test_deterministic():
+    S, Hq, Hkv, d, di, k, b = 900, 8, 2, 128, 128, 128, 64
+    say("determinism")
+    inp = make_inputs(S, Hq, Hkv, d, index_dim=di, dtype="bf16", needles=8, seed=4)
+    p = B.Problem(S, Hq, Hkv, d, index_dim=di, topk=k, block_q=b)
+    args = [cuda(x) for x in (inp.q, inp.k, inp.v, inp.q_idx, inp.k_idx)]
+    a = PL.indexer_prefill(p, *args)
+    o1, i1, s1 = a.o.clone(), a.idx.clone(), a.scores.clone()
+    PL.indexer_prefill(p, *args, buf=a)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, a.o) and torch.equal(i1, a.idx)
+    assert torch.equal(s1.nan_to_num(0), a.scores.nan_to_num(0))
+
+
+# ------------------------------------------------------- named workloads, full size
+def _units_for(p, inp, rng, n_random=3):
+    R = p.num_blocks
+    b = p.block_q
+    probes = [int(r) // b for r in inp.probe_query[:3]]
+    rand = rng.choice(R, size=min(n_random, R), replace=False).tolist()
+    return sorted(set([0, 1, R // 2, R - 1] + probes + rand))
+
+
+WORKLOAD_CASES = [
+    ("indexer_4k", 1, "max", False),
+    ("block_16k", 64, "sum", False),
+    ("block_16k", 64, "max", False),
+    ("headline_32k", 64, "max", False),
+    ("headline_32k", 1, "max", False),
+    ("stress_100k", 128, "max", False),
+    ("stress_100k", 128, "max", True),
+]
+
+
+@pytest.mark.parametrize("name,b,agg,untrained", WORKLOAD_CASES,
+                         ids=lambda c: str(c))
+def test_workload_indexer_mode(name, b, agg, untrained):
+    w = get_workload(name)
+    say(f"workload {name} b={b} agg={agg} untrained={untrained}")
+    inp = make_inputs(w.seq_len, w.num_q_heads, w.num_kv_heads, w.head_dim,
+                      index_dim=w.index_dim, dtype=w.dtype, needles=w.needles,
+                      stratified=w.stratified, seed=w.seed, untrained=untrained)
+    p = B.Problem(w.seq_len, w.num_q_heads, w.num_kv_heads, w.head_dim, index_dim=w.index_dim,
+                  topk=w.topk, block_q=b, local_window=w.local_window, agg=agg, dtype=w.dtype)
+    dev = inp.to("cuda")
+    buf = PL.indexer_prefill(p, dev.q, dev.k, dev.v, dev.q_idx, dev.k_idx)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(w.seed)
+    units = _units_for(p, inp, rng)
+    check_pipeline(p, inp, buf, "indexer", units, rows_per_unit=8,
+                   want_needles=not untrained)
+
+
+@pytest.mark.parametrize("name", ["indexer_4k", "headline_32k"])
+def test_workload_dense_sampled(name):
+    w = get_workload(name)
+    say(f"dense workload {name}")
+    inp = make_inputs(w.seq_len, w.num_q_heads, w.num_kv_heads, w.head_dim, dtype=w.dtype,
+                      needles=w.needles, seed=w.seed)
+    p = B.Problem(w.seq_len, w.num_q_heads, w.num_kv_heads, w.head_dim, dtype=w.dtype)
+    dev = inp.to("cuda")
+    lse = torch.empty(w.seq_len, w.num_q_heads, device="cuda")
+    o = PL.dense_prefill(p, dev.q, dev.k, dev.v, lse=lse)
+    torch.cuda.synchronize()
+    S = w.seq_len
+    rows = sorted(set([0, 1, 63, 64, S // 3, S // 2, S - 65, S - 1]))
+    ref_o, ref_lse = oracle.dense(inp.q, inp.k, inp.v, rows=rows)
+    ri = torch.as_tensor(rows, device="cuda")
+    eo, el = max_err(f64(o[ri]), ref_o), max_err(f64(lse[ri]), ref_lse)
+    say(f"  o err {eo:.3e} lse err {el:.3e}")
+    assert eo <= 2e-2 and el <= 1e-3
+
+
+def test_workload_oracle_mode_headline_sampled():
+    w = get_workload("headline_32k")
+    say("oracle mode headline_32k per-query, sampled rows")
+    inp = make_inputs(w.seq_len, w.num_q_heads, w.num_kv_heads, w.head_dim, dtype=w.dtype,
+                      needles=w.needles, seed=w.seed)
+    p = B.Problem(w.seq_len, w.num_q_heads, w.num_kv_heads, w.head_dim, topk=w.topk,
+                  block_q=1, dtype=w.dtype)
+    dev = inp.to("cuda")
+    buf = PL.oracle_prefill(p, dev.q, dev.k, dev.v)
+    torch.cuda.synchronize()
+    S = w.seq_len
+    units = sorted(set([0, 2047, 2048, 2049, S // 2, S - 1] +
+                       [int(r) for r in inp.probe_query[:2]]))
+    check_pipeline(p, inp, buf, "oracle", units, want_needles=False)
