@@ -143,6 +143,8 @@ int sp_indexer_scores(const sp_problem *p, const void *q_idx, const void *k_idx,
   if (!aligned16(q_idx) || !aligned16(k_idx) || !aligned16(scores)) return SP_ERR_ALIGN;
   SP_TRY(check_device());
   const Prob r = resolve(p);
+  if (indexer_mfma_supported(r))
+    return launched(launch_indexer_mfma(r, q_idx, k_idx, scores, stream));
   return launched(launch_indexer_rowwise(r, q_idx, k_idx, scores, stream));
 }
 
@@ -170,6 +172,8 @@ int sp_sparse_gqa_attn(const sp_problem *p, const void *q, const void *k, const 
     return SP_ERR_ALIGN;
   SP_TRY(check_device());
   const Prob r = resolve(p);
+  if (sparse_block_mfma_supported(r))
+    return launched(launch_sparse_block_mfma(r, q, k, v, idx, o, stream));
   return launched(launch_attn_rowwise(r, q, k, v, idx, o, nullptr, stream));
 }
 

@@ -21,6 +21,12 @@ struct Prob {
 hipError_t launch_attn_rowwise(const Prob &p, const void *q, const void *k, const void *v,
                                const int32_t *idx, void *o, float *lse, hipStream_t st);
 
+// bf16 MFMA sparse attention for selection blocks of b >= 16 queries: each
+// gathered K/V row is shared by the b*G query rows of a KV head.
+bool sparse_block_mfma_supported(const Prob &p);
+hipError_t launch_sparse_block_mfma(const Prob &p, const void *q, const void *k, const void *v,
+                                    const int32_t *idx, void *o, hipStream_t st);
+
 // Head-averaged mass with block aggregation.
 hipError_t launch_mass_rowwise(const Prob &p, const void *q, const void *k, const float *lse,
                                float *mass, hipStream_t st);
@@ -28,6 +34,12 @@ hipError_t launch_mass_rowwise(const Prob &p, const void *q, const void *k, cons
 // Indexer scores with block aggregation.
 hipError_t launch_indexer_rowwise(const Prob &p, const void *qi, const void *ki, float *scores,
                                   hipStream_t st);
+
+// bf16 MFMA indexer scores: b = 1 stores every causal score, b in
+// {16, 32, 64, 128} reduces over each selection block in the epilogue.
+bool indexer_mfma_supported(const Prob &p);
+hipError_t launch_indexer_mfma(const Prob &p, const void *qi, const void *ki, float *scores,
+                               hipStream_t st);
 
 // Row-wise top-k selection.
 hipError_t launch_topk(const Prob &p, const float *scores, int32_t *idx, hipStream_t st);

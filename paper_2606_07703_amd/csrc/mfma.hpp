@@ -1,0 +1,41 @@
+// gfx950 bf16 MFMA fragments.
+//
+// v_mfma_f32_16x16x32_bf16, for C[16x16] += A[16x32] * B[32x16], with lane
+// l (0..63), g = l/16:
+//   A: lane l holds row l%16, columns 8g..8g+7 (8 bf16, 16 bytes)
+//   B: lane l holds column l%16, rows 8g..8g+7
+//   C: lane l holds column l%16, rows 4g..4g+3 (4 floats)
+// These layouts were checked on the device against a host matmul.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sp {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma16(const bf16x8 &a, const bf16x8 &b, const f32x4 &c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(const uint4 &u) {
+  bf16x8 r;
+  __builtin_memcpy(&r, &u, sizeof(r));
+  return r;
+}
+
+__device__ __forceinline__ uint4 ldg16(const void *p) {
+  return *reinterpret_cast<const uint4 *>(p);
+}
+
+__device__ __forceinline__ uint4 lds16(const void *p) {
+  return *reinterpret_cast<const uint4 *>(p);
+}
+
+__device__ __forceinline__ void sts16(void *p, const uint4 &v) {
+  *reinterpret_cast<uint4 *>(p) = v;
+}
+
+}  // namespace sp

@@ -62,10 +62,12 @@ def test_sparse_attention(case):
     assert err <= tol_for(dtype)
 
 
-def test_sparse_attention_order_and_sentinels():
-    S, Hq, Hkv, d, b, k = 300, 8, 2, 128, 16, 64
-    say("sparse shuffled support")
-    inp = _inp(S, Hq, Hkv, d, dtype="f32", seed=5, peaked=True)
+@pytest.mark.parametrize("dtype,b,d", [("f32", 16, 128), ("bf16", 64, 128), ("bf16", 16, 64),
+                                       ("bf16", 128, 128)])
+def test_sparse_attention_order_and_sentinels(dtype, b, d):
+    S, Hq, Hkv, k = 300, 8, 2, 64
+    say(f"sparse shuffled support {dtype} b={b} d={d}")
+    inp = _inp(S, Hq, Hkv, d, dtype=dtype, seed=5, peaked=True)
     idx = make_support(S, b, k, seed=1)
     rng = np.random.default_rng(0)
     shuf = torch.from_numpy(np.stack([rng.permutation(r) for r in idx.numpy()]))
@@ -73,12 +75,14 @@ def test_sparse_attention_order_and_sentinels():
                      torch.full((shuf.shape[0], 3), S + 50, dtype=torch.int32)], dim=1)
     outs = []
     for table in (idx, pad):
-        p = B.Problem(S, Hq, Hkv, d, topk=table.shape[1], block_q=b, dtype="f32")
-        o = torch.empty(S, Hq, d, device="cuda")
+        p = B.Problem(S, Hq, Hkv, d, topk=table.shape[1], block_q=b, dtype=dtype)
+        o = torch.empty(S, Hq, d, dtype=inp.q.dtype, device="cuda")
         B.sp_sparse_gqa_attn(p, cuda(inp.q), cuda(inp.k), cuda(inp.v), cuda(table.contiguous()),
                              o)
         outs.append(f64(o))
-    assert max_err(outs[0], outs[1]) < 1e-6
+    assert max_err(outs[0], outs[1]) < (1e-6 if dtype == "f32" else 1e-2)
+    ref = oracle.sparse(inp.q, inp.k, inp.v, idx, b)
+    assert max_err(outs[1], ref) <= tol_for(dtype)
 
 
 # ----------------------------------------------------------------------- dense
@@ -151,6 +155,8 @@ def test_topk(case):
 INDEXER_CASES = [
     # S, d_idx, b, agg, relu, dtype
     (300, 64, 1, "max", 1, "bf16"),
+    (301, 128, 1, "max", 1, "bf16"),
+    (1100, 128, 1, "max", 0, "bf16"),
     (300, 128, 16, "max", 1, "bf16"),
     (300, 128, 64, "sum", 1, "bf16"),
     (300, 256, 64, "max", 0, "bf16"),
