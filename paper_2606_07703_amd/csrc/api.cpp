@@ -115,6 +115,7 @@ int sp_dense_attn(const sp_problem *p, const void *q, const void *k, const void 
     return SP_ERR_ALIGN;
   SP_TRY(check_device());
   const Prob r = resolve(p);
+  if (dense_mfma_supported(r)) return launched(launch_dense_mfma(r, q, k, v, o, lse, stream));
   return launched(launch_attn_rowwise(r, q, k, v, nullptr, o, lse, stream));
 }
 
@@ -128,6 +129,7 @@ int sp_oracle_support(const sp_problem *p, const void *q, const void *k, const f
   if (!aligned16(q) || !aligned16(k) || !aligned16(lse) || !aligned16(mass)) return SP_ERR_ALIGN;
   SP_TRY(check_device());
   const Prob r = resolve(p);
+  if (mass_mfma_supported(r)) return launched(launch_mass_mfma(r, q, k, lse, mass, stream));
   return launched(launch_mass_rowwise(r, q, k, lse, mass, stream));
 }
 

@@ -27,9 +27,17 @@ bool sparse_block_mfma_supported(const Prob &p);
 hipError_t launch_sparse_block_mfma(const Prob &p, const void *q, const void *k, const void *v,
                                     const int32_t *idx, void *o, hipStream_t st);
 
+// bf16 MFMA causal flash attention; o and/or lse (o == nullptr: normalisers only).
+bool dense_mfma_supported(const Prob &p);
+hipError_t launch_dense_mfma(const Prob &p, const void *q, const void *k, const void *v,
+                             void *o, float *lse, hipStream_t st);
+
 // Head-averaged mass with block aggregation.
 hipError_t launch_mass_rowwise(const Prob &p, const void *q, const void *k, const float *lse,
                                float *mass, hipStream_t st);
+bool mass_mfma_supported(const Prob &p);
+hipError_t launch_mass_mfma(const Prob &p, const void *q, const void *k, const float *lse,
+                            float *mass, hipStream_t st);
 
 // Indexer scores with block aggregation.
 hipError_t launch_indexer_rowwise(const Prob &p, const void *qi, const void *ki, float *scores,

@@ -93,6 +93,9 @@ DENSE_CASES = [
     (300, 8, 2, 128, "bf16"),
     (515, 32, 8, 128, "bf16"),
     (260, 4, 4, 64, "bf16"),
+    (333, 8, 8, 128, "bf16"),
+    (333, 8, 1, 64, "bf16"),
+    (1100, 32, 8, 128, "bf16"),
 ]
 
 
@@ -194,6 +197,9 @@ MASS_CASES = [
     (300, 8, 2, 128, 64, "max", "bf16"),
     (300, 8, 2, 128, 16, "sum", "bf16"),
     (260, 32, 8, 128, 1, "max", "bf16"),
+    (300, 16, 4, 64, 32, "sum", "bf16"),
+    (1000, 32, 8, 128, 128, "max", "bf16"),
+    (200, 8, 1, 64, 1, "max", "bf16"),
 ]
 
 
