@@ -46,7 +46,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="headline_32k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-units", type=int, default=24,
+    ap.add_argument("--cpu-units", type=int, default=256,
                     help="selection blocks the CPU oracle times (bounded sample)")
     return ap.parse_args()
 

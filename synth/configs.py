@@ -4,7 +4,7 @@ Each workload is a synthetic, Qwen-like GQA layer: sequence length S, query
 heads Hq, KV heads Hkv, head dim d, indexer dim d_idx, top-k budget k,
 selection-block size b_sel, forced local window W, block aggregation rule and
 storage dtype. Budgets and lengths follow the paper's evaluated ranges
-(Section 5.1: 4K..100K contexts, top-k 256..2048; Section 7.3: top-k up to 1024
+(Section 5.1: 4K..100K contexts, top-k 256..2048; Section 8, Finding 3: top-k up to 1024
 at 32K; b_sel in {1, 64} in Section 5.1). "100K" is 102,400 tokens: only that
 length reproduces the 96.0% causal sparsity printed in Table 2.
 """
