@@ -22,6 +22,8 @@
 namespace sp {
 namespace {
 
+constexpr float kLazy = 8.f;
+
 template <typename T, int D, int HPW, bool SPARSE>
 __global__ __launch_bounds__(64) void attn_rowwise_kernel(
     int S, int Hq, int Hkv, int G, float scale_log2, const T *__restrict__ q,
@@ -70,15 +72,21 @@ __global__ __launch_bounds__(64) void attn_rowwise_kernel(
       float part = 0.f;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) part = fmaf(qr[hh][e], kf[e], part);
-      float x = group_sum<16>(part);
+      const float x = row16_sum(part);
       if (valid) {
-        const float mn = fmaxf(m[hh], x);
-        const float corr = exp2f(m[hh] - mn);  // m = -inf gives 0
-        const float pr = exp2f(x - mn);
-        l[hh] = l[hh] * corr + pr;
+        // The running max moves only when a logit exceeds it by 2^kLazy, so
+        // the accumulator is rescaled rarely (probabilities stay <= 2^kLazy).
+        if (x > m[hh] + kLazy) {
+          const float corr = __builtin_amdgcn_exp2f(m[hh] - x);  // m = -inf gives 0
+          l[hh] *= corr;
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[hh][e] = fmaf(acc[hh][e], corr, pr * vf[e]);
-        m[hh] = mn;
+          for (int e = 0; e < EPL; ++e) acc[hh][e] *= corr;
+          m[hh] = x;
+        }
+        const float pr = __builtin_amdgcn_exp2f(x - m[hh]);
+        l[hh] += pr;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[hh][e] = fmaf(pr, vf[e], acc[hh][e]);
       }
     }
   }

@@ -2,17 +2,25 @@
 //
 // A workgroup owns up to 256 query rows ((query, head) pairs of one KV head,
 // 32 per wave) and walks a list of key positions in tiles of 64. For each
-// tile it stages K (row-major, padded rows) and V (transposed, d-major) of
-// the KV head in LDS, plus the tile's positions. attn_tile() then updates
-// each lane's online-softmax state: scores are computed transposed,
-// S^T = K Q^T, so lane (g, c16) owns query row c16 of each 16-row tile and
-// holds keys 16*kt + 4g + r; the output is kept transposed too,
-// O^T = V^T P^T, so the per-row rescale stays in the lane.
+// tile it stages K and V of the KV head in LDS (both row-major, padded rows),
+// plus the tile's positions and their min/max. attn_tile() then updates each
+// lane's online-softmax state: scores are computed transposed, S^T = K Q^T,
+// so lane (g, c16) owns query row c16 of each 16-row tile and holds keys
+// 16*kt + 4g + r; the output is kept transposed too, O^T = V^T P^T, with the
+// V^T operand read straight from the row-major V tile by the gfx950 LDS
+// transpose read (ds_read_b64_tr_b16), so the per-row rescale stays in the
+// lane and no transposed copy of V is ever written.
 //
 // A key at position s contributes to a row of query t only if
-// 0 <= s <= t and s < S (the causal mask of Section 3, applied per query as
-// in Section 4.2); any other position (e.g. a -1 sentinel) contributes
-// nothing.
+// 0 <= s <= t (the causal mask of Section 3, applied per query as in
+// Section 4.2); any other position (e.g. a -1 sentinel) contributes nothing.
+// A wave skips the mask test on tiles whose positions all lie in
+// [0, first query of the wave].
+//
+// The running row maximum is raised only when a tile's maximum exceeds it by
+// more than 2^kLazy in the exponent base-2 domain; until then the stale
+// maximum is kept (probabilities up to 2^kLazy are exact in fp32 and bf16
+// range), so the output accumulators are rescaled only when it moves.
 #pragma once
 
 #include <math.h>
@@ -22,31 +30,35 @@
 
 namespace sp {
 
-constexpr int kAttnKT = 64;    // key positions per tile
-constexpr int kAttnQPW = 32;   // query rows per wave
+constexpr int kAttnKT = 64;      // key positions per tile
+constexpr int kAttnQPW = 32;     // query rows per wave
+constexpr float kLazy = 8.f;     // max may lag by up to 8 (factor 256)
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
 
 template <int D>
 struct AttnLayout {
-  static constexpr int KRB = D * 2 + 16;   // K row bytes, padded: 16 lanes hit distinct banks
-  static constexpr int VTS = 72;           // V^T row stride (elements): conflict-free b64 reads
+  static constexpr int KRB = D * 2 + 16;   // K row bytes: 16 lanes x 16 B on distinct banks
+  static constexpr int VRB = D * 2 + 32;   // V row bytes: conflict-free transpose reads
   static constexpr int KBYTES = kAttnKT * KRB;
-  static constexpr int VBYTES = D * VTS * 2;
-  static constexpr int BUF = KBYTES + VBYTES + kAttnKT * 4;
+  static constexpr int VBYTES = kAttnKT * VRB;
+  static constexpr int POS = KBYTES + VBYTES;          // int positions[64], then min, max
+  static constexpr int BUF = POS + kAttnKT * 4 + 16;
   static constexpr int KS = D / 32;        // k-steps of K Q^T
   static constexpr int DT = D / 16;        // 16-row tiles of O^T
 };
 
-// Global -> registers -> LDS staging of one tile of K, V^T and positions.
-// POS(c) gives the position of tile entry c (0..63), or a negative value.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Global -> registers -> LDS staging of one tile of K, V and positions.
+// pos(e) gives the position of tile entry e (0..63), or a negative value.
 template <int D, int NT, bool WANT_V>
 struct KVStage {
   using L = AttnLayout<D>;
-  static constexpr int KPIECES = kAttnKT * D / 8;
-  static constexpr int KPER = (KPIECES + NT - 1) / NT;
-  static constexpr int VUNITS = (kAttnKT / 4) * (D / 4);
-  static constexpr int VPER = WANT_V ? (VUNITS + NT - 1) / NT : 0;
-  uint4 kreg[KPER];
-  uint2 vreg[VPER > 0 ? VPER : 1][4];
+  static constexpr int PIECES = kAttnKT * D / 8;    // 16-byte pieces of one tile
+  static constexpr int PER = (PIECES + NT - 1) / NT;
+  uint4 kreg[PER];
+  uint4 vreg[WANT_V ? PER : 1];
   int spos;
 
   template <typename POS>
@@ -54,68 +66,45 @@ struct KVStage {
                                        const uint16_t *__restrict__ v, int S, int Hkv, int j,
                                        int tid, POS pos) {
 #pragma unroll
-    for (int i = 0; i < KPER; ++i) {
+    for (int i = 0; i < PER; ++i) {
       const int c = tid + i * NT;
-      if (c < KPIECES) {
+      if (c < PIECES) {
         const int key = c / (D / 8), col = c % (D / 8);
         int s = pos(key);
         s = (s >= 0 && s < S) ? s : 0;
-        kreg[i] = ldg16(k + ((size_t)s * Hkv + j) * D + col * 8);
-      }
-    }
-    if constexpr (WANT_V) {
-#pragma unroll
-      for (int i = 0; i < VPER; ++i) {
-        const int u = tid + i * NT;
-        if (u < VUNITS) {
-          const int kq = u / (D / 4), dq = u % (D / 4);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            int s = pos(kq * 4 + e);
-            s = (s >= 0 && s < S) ? s : 0;
-            vreg[i][e] = *reinterpret_cast<const uint2 *>(v + ((size_t)s * Hkv + j) * D + dq * 4);
-          }
-        }
+        const size_t off = ((size_t)s * Hkv + j) * D + col * 8;
+        kreg[i] = ldg16(k + off);
+        if constexpr (WANT_V) vreg[i] = ldg16(v + off);
       }
     }
     if (tid < kAttnKT) spos = pos(tid);
   }
 
+  // Also publishes min and max of the tile's positions (wave 0 holds them).
   __device__ __forceinline__ void store(char *buf, int tid) const {
-    char *kl = buf;
 #pragma unroll
-    for (int i = 0; i < KPER; ++i) {
+    for (int i = 0; i < PER; ++i) {
       const int c = tid + i * NT;
-      if (c < KPIECES) {
+      if (c < PIECES) {
         const int key = c / (D / 8), col = c % (D / 8);
-        sts16(kl + key * L::KRB + col * 16, kreg[i]);
+        sts16(buf + key * L::KRB + col * 16, kreg[i]);
+        if constexpr (WANT_V) sts16(buf + L::KBYTES + key * L::VRB + col * 16, vreg[i]);
       }
     }
-    if constexpr (WANT_V) {
-      uint16_t *vt = reinterpret_cast<uint16_t *>(buf + L::KBYTES);
+    if (tid < kAttnKT) {
+      int *pl = reinterpret_cast<int *>(buf + L::POS);
+      pl[tid] = spos;
+      int mn = spos, mx = spos;
 #pragma unroll
-      for (int i = 0; i < VPER; ++i) {
-        const int u = tid + i * NT;
-        if (u < VUNITS) {
-          const int kq = u / (D / 4), dq = u % (D / 4);
-          // vreg[i][e] holds d = 4dq..4dq+3 of key 4kq+e; write one d row at a time.
-#pragma unroll
-          for (int dd = 0; dd < 4; ++dd) {
-            uint32_t w[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const uint32_t word = (dd < 2) ? vreg[i][e].x : vreg[i][e].y;
-              w[e] = (dd & 1) ? (word >> 16) : (word & 0xffffu);
-            }
-            uint2 packed;
-            packed.x = w[0] | (w[1] << 16);
-            packed.y = w[2] | (w[3] << 16);
-            *reinterpret_cast<uint2 *>(vt + (dq * 4 + dd) * L::VTS + kq * 4) = packed;
-          }
-        }
+      for (int off = 32; off > 0; off >>= 1) {
+        mn = min(mn, __shfl_xor(mn, off, 64));
+        mx = max(mx, __shfl_xor(mx, off, 64));
+      }
+      if (tid == 0) {
+        pl[kAttnKT] = mn;
+        pl[kAttnKT + 1] = mx;
       }
     }
-    if (tid < kAttnKT) reinterpret_cast<int *>(buf + L::KBYTES + L::VBYTES)[tid] = spos;
   }
 };
 
@@ -123,7 +112,7 @@ struct KVStage {
 template <int D>
 struct AttnState {
   f32x4 oacc[AttnLayout<D>::DT][2];
-  float m[2];
+  float m[2];   // running max (base-2 scaled logits), possibly lagging by < kLazy
   float l[2];   // this lane's share of the row sum (reduce over g at the end)
   __device__ __forceinline__ void init() {
 #pragma unroll
@@ -136,16 +125,17 @@ struct AttnState {
 };
 
 // One tile: scores, mask, online softmax, and (WANT_O) the P V product.
-// mask = false promises every staged position p satisfies 0 <= p <= qt.
+// wave_tmin is the smallest query of the wave's valid rows.
 template <int D, bool WANT_O>
 __device__ __forceinline__ void attn_tile(const char *buf, const bf16x8 (&bq)[2][AttnLayout<D>::KS],
-                                          const int (&qt)[2], float scale_log2, bool mask,
+                                          const int (&qt)[2], float scale_log2, int wave_tmin,
                                           AttnState<D> &st, int g, int c16) {
   using L = AttnLayout<D>;
   constexpr int KS = L::KS, DT = L::DT;
   const char *kl = buf;
-  const uint16_t *vt = reinterpret_cast<const uint16_t *>(buf + L::KBYTES);
-  const int *sl = reinterpret_cast<const int *>(buf + L::KBYTES + L::VBYTES);
+  const char *vl = buf + L::KBYTES;
+  const int *sl = reinterpret_cast<const int *>(buf + L::POS);
+  const bool mask = !(sl[kAttnKT] >= 0 && sl[kAttnKT + 1] <= wave_tmin);
   f32x4 sacc[4][2];
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt) {
@@ -158,28 +148,37 @@ __device__ __forceinline__ void attn_tile(const char *buf, const bf16x8 (&bq)[2]
       for (int qc = 0; qc < 2; ++qc) sacc[kt][qc] = mfma16(a, bq[qc][ks], sacc[kt][qc]);
     }
   }
-  bf16x8 pfrag[2][2];
-#pragma unroll
-  for (int qc = 0; qc < 2; ++qc) {
-    float x[4][4];
-    float tmax = -INFINITY;
+  if (mask) {
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
-      int4 s4 = make_int4(0, 0, 0, 0);
-      if (mask) s4 = *reinterpret_cast<const int4 *>(sl + kt * 16 + g * 4);
+      const int4 s4 = *reinterpret_cast<const int4 *>(sl + kt * 16 + g * 4);
       const int sv[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const bool ok = !mask || (sv[rr] >= 0 && sv[rr] <= qt[qc]);
-        x[kt][rr] = ok ? sacc[kt][qc][rr] * scale_log2 : -INFINITY;
-        tmax = fmaxf(tmax, x[kt][rr]);
-      }
+      for (int qc = 0; qc < 2; ++qc)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+          if (!(sv[rr] >= 0 && sv[rr] <= qt[qc])) sacc[kt][qc][rr] = -INFINITY;
     }
+  }
+  bf16x8 pfrag[2][2];
+  bool grew_any = false;
+  float corr[2];
+#pragma unroll
+  for (int qc = 0; qc < 2; ++qc) {
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) tmax = fmaxf(tmax, sacc[kt][qc][rr]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float mnew = fmaxf(st.m[qc], tmax);
+    tmax *= scale_log2;   // scale > 0 commutes with max
+    const float mold = st.m[qc];
+    const bool grow = tmax > mold + kLazy;
+    const float mnew = grow ? tmax : mold;
+    grew_any |= grow;
     const float mref = mnew == -INFINITY ? 0.f : mnew;
-    const float corr = exp2f(st.m[qc] - mref);
+    corr[qc] = fast_exp2(mold - mref);   // mold = -inf gives 0; unchanged gives 1
     st.m[qc] = mnew;
     float psum = 0.f;
     float pv[4][4];
@@ -187,15 +186,11 @@ __device__ __forceinline__ void attn_tile(const char *buf, const bf16x8 (&bq)[2]
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
-        pv[kt][rr] = exp2f(x[kt][rr] - mref);
+        pv[kt][rr] = fast_exp2(fmaf(sacc[kt][qc][rr], scale_log2, -mref));
         psum += pv[kt][rr];
       }
-    st.l[qc] = st.l[qc] * corr + psum;
+    st.l[qc] = st.l[qc] * corr[qc] + psum;
     if constexpr (WANT_O) {
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) st.oacc[dt][qc][rr] *= corr;
 #pragma unroll
       for (int f = 0; f < 2; ++f) {
         bf16x8 pf;
@@ -209,16 +204,30 @@ __device__ __forceinline__ void attn_tile(const char *buf, const bf16x8 (&bq)[2]
     }
   }
   if constexpr (WANT_O) {
+    if (__any(grew_any)) {
+#pragma unroll
+      for (int qc = 0; qc < 2; ++qc)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) st.oacc[dt][qc][rr] *= corr[qc];
+    }
+    // O^T += V^T P^T. Lane (g, c16) of the V^T fragment needs d = 16dt + c16
+    // and keys 32f + 4g + {0..3} (then +16): each transpose read has the 16
+    // lanes of group g point at rows 32f + 4g + c16/4 (+16), d = 16dt + 4(c16%4).
+    const char *vbase = vl + (g * 4 + (c16 >> 2)) * L::VRB + (c16 & 3) * 8;
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const uint16_t *vrow = vt + (dt * 16 + c16) * L::VTS + f * 32 + g * 4;
-        const uint2 lo = *reinterpret_cast<const uint2 *>(vrow);
-        const uint2 hi = *reinterpret_cast<const uint2 *>(vrow + 16);
-        uint4 u;
-        u.x = lo.x; u.y = lo.y; u.z = hi.x; u.w = hi.y;
-        const bf16x8 a = as_bf16x8(u);
+        const char *p0 = vbase + (f * 32) * L::VRB + dt * 32;
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4i16 *)(size_t)(p0));
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4i16 *)(size_t)(p0 + 16 * L::VRB));
+        bf16x8 a;
+        __builtin_memcpy(&a, &lo, 8);
+        __builtin_memcpy(reinterpret_cast<char *>(&a) + 8, &hi, 8);
 #pragma unroll
         for (int qc = 0; qc < 2; ++qc) st.oacc[dt][qc] = mfma16(a, pfrag[qc][f], st.oacc[dt][qc]);
       }

@@ -98,6 +98,17 @@ __device__ __forceinline__ float group_sum(float x) {
   return x;
 }
 
+// Sum over each 16-lane row with DPP lane moves (no LDS traffic): swap
+// neighbours, swap pairs, then rotate the row by 4 and by 8; every lane ends
+// with its row's total.
+__device__ __forceinline__ float row16_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x124, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, false));
+  return x;
+}
+
 // Order-preserving map float -> uint32 (larger float, larger key); -0.0 and
 // +0.0 share one key.
 __device__ __forceinline__ uint32_t float_key(float f) {

@@ -4,8 +4,8 @@
 //
 // One workgroup per (tile of 256/G queries, KV head j): its 256 query rows are
 // every (query, head) pair of the tile with g(h) = j, so each K/V tile staged
-// in LDS serves all G heads of the group. Key tiles strictly below the
-// query tile need no mask; only tiles reaching the diagonal apply s <= t.
+// in LDS serves all G heads of the group. Key tiles below a wave's first
+// query need no mask; only tiles reaching the diagonal apply s <= t.
 // Query tiles are scheduled longest first (the causal work of tile i grows
 // with i), which shortens the tail of the launch.
 //
@@ -46,7 +46,6 @@ __global__ __launch_bounds__(kNW * 64) void dense_fwd_kernel(
   st.init();
   KVStage<D, NT, WANT_O> stage;
   const int ntiles = tl / kAttnKT + 1;
-  const int first_masked = t0 / kAttnKT;
   auto pos_of = [&](int base) {
     return [=](int e) { return base + e < S ? base + e : -1; };
   };
@@ -54,10 +53,11 @@ __global__ __launch_bounds__(kNW * 64) void dense_fwd_kernel(
   stage.store(lds[0], tid);
   __syncthreads();
   const bool live = row0 < nrows;
+  const int wave_tmin = t0 + row0 / G;
   for (int it = 0; it < ntiles; ++it) {
     const bool more = it + 1 < ntiles;
     if (more) stage.load(k, v, S, Hkv, j, tid, pos_of((it + 1) * kAttnKT));
-    if (live) attn_tile<D, WANT_O>(lds[it & 1], bq, qt, scale_log2, it >= first_masked, st, g, c16);
+    if (live) attn_tile<D, WANT_O>(lds[it & 1], bq, qt, scale_log2, wave_tmin, st, g, c16);
     if (more) stage.store(lds[(it + 1) & 1], tid);
     __syncthreads();
   }

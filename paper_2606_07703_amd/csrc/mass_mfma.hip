@@ -130,7 +130,8 @@ __global__ __launch_bounds__(kNW * 64) void mass_kernel(
             acc = mfma16(a, bqf[hh][ks], acc);
           }
 #pragma unroll
-          for (int r = 0; r < 4; ++r) part[ks2][r] += exp2f(acc[r] * scale_log2 - lse2[hh]);
+          for (int r = 0; r < 4; ++r)
+            part[ks2][r] += __builtin_amdgcn_exp2f(fmaf(acc[r], scale_log2, -lse2[hh]));
         }
       }
 #pragma unroll

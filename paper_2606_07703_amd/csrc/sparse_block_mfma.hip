@@ -69,10 +69,11 @@ __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
   }
   __syncthreads();
   const bool live = row0 < nrows;
+  const int wave_tmin = t0 + row0 / G;
   for (int it = 0; it < ntiles; ++it) {
     const bool more = it + 1 < ntiles;
     if (more) stage.load(k, v, S, Hkv, j, tid, pos_of((it + 1) * kAttnKT));
-    if (live) attn_tile<D, true>(lds[it & 1], bq, qt, scale_log2, true, st, g, c16);
+    if (live) attn_tile<D, true>(lds[it & 1], bq, qt, scale_log2, wave_tmin, st, g, c16);
     if (more) stage.store(lds[(it + 1) & 1], tid);
     __syncthreads();
   }
