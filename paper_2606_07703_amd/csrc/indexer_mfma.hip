@@ -68,7 +68,11 @@ __device__ __forceinline__ float agg2(int agg, float a, float b) {
   return agg == SP_AGG_MAX ? fmaxf(a, b) : a + b;
 }
 
-template <int DI, int BQ>
+// MAXPOS: aggregation is max and the scale is non-negative, so scale and
+// ReLU commute with the max: rows are reduced on raw MFMA outputs and only
+// the reduced value is scaled; tiles entirely below a wave's first query
+// skip the causal test.
+template <int DI, int BQ, bool MAXPOS>
 __global__ __launch_bounds__(512) void indexer_block_kernel(int S, int agg, int relu,
                                                             float scale,
                                                             const uint16_t *__restrict__ qi,
@@ -132,24 +136,52 @@ __global__ __launch_bounds__(512) void indexer_block_kernel(int S, int agg, int 
 #pragma unroll
           for (int rt = 0; rt < 4; ++rt) acc[rt] = mfma16(a[rt][ks], b, acc[rt]);
         }
+        if constexpr (MAXPOS) {
+          const bool full = kt0 + KT - 1 <= qw0 && qw0 + kQW - 1 <= qw_last;
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) {
-          float m = neutral;
+          for (int rt = 0; rt < 4; ++rt) {
+            float m;
+            if (full) {
+              m = fmaxf(fmaxf(acc[rt][0], acc[rt][1]), fmaxf(acc[rt][2], acc[rt][3]));
+            } else {
+              m = -INFINITY;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int t = qw0 + rt * 16 + g * 4 + r;
-            float x = acc[rt][r] * scale;
-            if (relu) x = x > 0.f ? x : 0.f;
-            m = agg2(agg, m, (t <= qw_last && s <= t) ? x : neutral);
+              for (int r = 0; r < 4; ++r) {
+                const int t = qw0 + rt * 16 + g * 4 + r;
+                m = fmaxf(m, (t <= qw_last && s <= t) ? acc[rt][r] : -INFINITY);
+              }
+            }
+            reduced[ct][rt / RPB] = fmaxf(reduced[ct][rt / RPB], m);
           }
-          reduced[ct][rt / RPB] = agg2(agg, reduced[ct][rt / RPB], m);
-        }
 #pragma unroll
-        for (int bb = 0; bb < BPW; ++bb) {
-          float m = reduced[ct][bb];
-          m = agg2(agg, m, __shfl_xor(m, 16, 64));
-          m = agg2(agg, m, __shfl_xor(m, 32, 64));
-          reduced[ct][bb] = m;
+          for (int bb = 0; bb < BPW; ++bb) {
+            float m = reduced[ct][bb];
+            m = fmaxf(m, __shfl_xor(m, 16, 64));
+            m = fmaxf(m, __shfl_xor(m, 32, 64));
+            m *= scale;
+            if (relu) m = fmaxf(m, 0.f);   // -inf (no causal row) becomes 0; never stored
+            reduced[ct][bb] = m;
+          }
+        } else {
+#pragma unroll
+          for (int rt = 0; rt < 4; ++rt) {
+            float m = neutral;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int t = qw0 + rt * 16 + g * 4 + r;
+              float x = acc[rt][r] * scale;
+              if (relu) x = x > 0.f ? x : 0.f;
+              m = agg2(agg, m, (t <= qw_last && s <= t) ? x : neutral);
+            }
+            reduced[ct][rt / RPB] = agg2(agg, reduced[ct][rt / RPB], m);
+          }
+#pragma unroll
+          for (int bb = 0; bb < BPW; ++bb) {
+            float m = reduced[ct][bb];
+            m = agg2(agg, m, __shfl_xor(m, 16, 64));
+            m = agg2(agg, m, __shfl_xor(m, 32, 64));
+            reduced[ct][bb] = m;
+          }
         }
       }
     }
@@ -287,9 +319,14 @@ hipError_t launch_di(const Prob &p, const void *qi, const void *ki, float *score
     return hipGetLastError();
   }
   dim3 grid((p.S + 511) / 512, (p.S + kKC - 1) / kKC);
+  const bool maxpos = p.agg == SP_AGG_MAX && p.iscale >= 0.f;
 #define SP_BLK(BQ)                                                                           \
-  hipLaunchKernelGGL((indexer_block_kernel<DI, BQ>), grid, dim3(512), 0, st, p.S, p.agg,     \
-                     p.relu, p.iscale, q, k, scores)
+  if (maxpos)                                                                                \
+    hipLaunchKernelGGL((indexer_block_kernel<DI, BQ, true>), grid, dim3(512), 0, st, p.S,    \
+                       p.agg, p.relu, p.iscale, q, k, scores);                               \
+  else                                                                                       \
+    hipLaunchKernelGGL((indexer_block_kernel<DI, BQ, false>), grid, dim3(512), 0, st, p.S,   \
+                       p.agg, p.relu, p.iscale, q, k, scores)
   switch (p.b) {
     case 16: SP_BLK(16); break;
     case 32: SP_BLK(32); break;

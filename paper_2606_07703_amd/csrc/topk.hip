@@ -6,33 +6,207 @@
 // other k' = k-Wf are chosen among positions [0, L-Wf) in the order
 // (score descending, position ascending).
 //
-// Keys are the order-preserving uint32 images of the fp32 scores. One
-// workgroup per row finds the exact k'-th largest key T with three radix
-// passes (12, 12 and 8 bits; LDS histograms; each pass counts only keys that
-// share the prefix fixed so far). The chosen set is then {key > T} plus the
-// first (k' - #{key > T}) positions with key == T. A final pass visits the
-// row in position order and compacts the chosen positions with block-wide
-// prefix sums, so every output row comes out ascending without a sort.
+// Keys are the order-preserving uint32 images of the fp32 scores (-0 and +0
+// share one key). One workgroup per row finds the exact k'-th largest key T
+// with three radix passes over LDS histograms (11, 11 and 10 bits; each pass
+// counts only keys sharing the prefix fixed so far). The chosen set is then
+// {key > T} plus the first (k' - #{key > T}) positions with key == T, and a
+// final ordered pass compacts the chosen positions with block-wide prefix
+// sums, so every output row comes out ascending without a sort.
+//
+// topk_reg_kernel keeps the row in registers (each thread owns runs of 16
+// consecutive positions) for rows of up to 32768 candidates; the exact zero
+// keys that ReLU produces in bulk are counted by wave ballots instead of
+// contended LDS atomics. topk_rows_kernel streams longer rows from memory on
+// every pass.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace sp {
 namespace {
 
-constexpr int kNT = 256;         // threads per workgroup
-constexpr int kEmitPer = 16;     // consecutive elements per thread in the emit pass
+constexpr uint32_t kZeroKey = 0x80000000u;   // float_key(+0.0f)
+
+__device__ __forceinline__ int digit_shift(int pass) { return pass == 0 ? 21 : (pass == 1 ? 10 : 0); }
+__device__ __forceinline__ int digit_bits(int pass) { return pass == 2 ? 10 : 11; }
+
+// Given a filled histogram of nb bins, find the bin holding the
+// `remaining`-th largest key; writes (bin, rank within bin) to sel.
+// Every thread must call it (it contains barriers).
+template <int NT>
+__device__ __forceinline__ void find_digit(const uint32_t *hist, int nb, uint32_t remaining,
+                                           uint32_t *scan_scratch, uint32_t *sel) {
+  const int tid = threadIdx.x;
+  const int per = nb / NT;            // nb is a multiple of NT
+  const int hi = nb - tid * per;      // thread 0 owns the highest bins
+  uint32_t mine = 0;
+  for (int i = hi - per; i < hi; ++i) mine += hist[i];
+  uint32_t total;
+  const uint32_t above = block_exclusive_scan<NT>(mine, scan_scratch, &total);
+  if (above < remaining && above + mine >= remaining) {
+    uint32_t acc = above;
+    for (int i = hi - 1; i >= hi - per; --i) {
+      const uint32_t c = hist[i];
+      if (acc + c >= remaining) {
+        sel[0] = (uint32_t)i;
+        sel[1] = remaining - acc;
+        break;
+      }
+      acc += c;
+    }
+  }
+  __syncthreads();
+}
+
+// ------------------------------------------------------------ register rows
+constexpr int kRegNT = 512;
+constexpr int kRun = 16;                      // consecutive positions per run
+constexpr int kRegSub = 4;                    // runs per thread
+constexpr int kRegCap = kRegNT * kRun * kRegSub;   // 32768 candidates
+
+__global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int b, int k, int W,
+                                                          const float *__restrict__ scores,
+                                                          int32_t *__restrict__ idx) {
+  constexpr int NT = kRegNT;
+  __shared__ uint32_t hist[2048];
+  __shared__ uint32_t scan_scratch[NT / 64 + 1];
+  __shared__ uint32_t sel[2];
+
+  const int r = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int t1 = min(r * b + b, S) - 1;
+  const int L = t1 + 1;
+  int32_t *out = idx + (size_t)r * k;
+  const float *row = scores + (size_t)r * S;
+  if (L <= k) {
+    for (int c = tid; c < k; c += NT) out[c] = c < L ? c : -1;
+    return;
+  }
+  const int Wf = min(W, k);
+  const int nc = L - Wf;
+  const int kp = k - Wf;
+  const int nsub = (nc + NT * kRun - 1) / (NT * kRun);   // runs in use (<= kRegSub)
+  const bool vec = ((((size_t)r * S) & 3) == 0);         // row start 16-byte aligned
+
+  // Run j of thread t covers positions [kRun*(t + NT*j), +kRun).
+  uint32_t key[kRegSub][kRun];
+#pragma unroll
+  for (int j = 0; j < kRegSub; ++j) {
+    const int p0 = kRun * (tid + NT * j);
+#pragma unroll
+    for (int i = 0; i < kRun; i += 4) {
+      float f[4] = {0.f, 0.f, 0.f, 0.f};
+      if (j < nsub) {
+        if (vec && p0 + i + 3 < nc) {
+          const float4 x = *reinterpret_cast<const float4 *>(row + p0 + i);
+          f[0] = x.x; f[1] = x.y; f[2] = x.z; f[3] = x.w;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (p0 + i + e < nc) f[e] = row[p0 + i + e];
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) key[j][i + e] = float_key(f[e]);
+    }
+  }
+
+  uint32_t T = 0xffffffffu, remaining = 0;
+  if (kp > 0) {
+    uint32_t prefix = 0, pmask = 0;
+    remaining = (uint32_t)kp;
+#pragma unroll 1
+    for (int pass = 0; pass < 3; ++pass) {
+      const int shift = digit_shift(pass), nb = 1 << digit_bits(pass);
+      const uint32_t dmask = (uint32_t)nb - 1u;
+      for (int i = tid; i < nb; i += NT) hist[i] = 0;
+      __syncthreads();
+      uint32_t zc = 0;
+#pragma unroll
+      for (int j = 0; j < kRegSub; ++j) {
+        if (j >= nsub) continue;
+        const int p0 = kRun * (tid + NT * j);
+#pragma unroll
+        for (int i = 0; i < kRun; ++i) {
+          const uint32_t kv = key[j][i];
+          if (p0 + i < nc && (kv & pmask) == prefix) {
+            if (kv == kZeroKey) ++zc;
+            else atomicAdd(&hist[(kv >> shift) & dmask], 1u);
+          }
+        }
+      }
+      if ((kZeroKey & pmask) == prefix) {
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) zc += __shfl_xor(zc, off, 64);
+        if (lane == 0 && zc) atomicAdd(&hist[(kZeroKey >> shift) & dmask], zc);
+      }
+      __syncthreads();
+      find_digit<NT>(hist, nb, remaining, scan_scratch, sel);
+      prefix |= sel[0] << shift;
+      pmask |= dmask << shift;
+      remaining = sel[1];
+      __syncthreads();
+    }
+    T = prefix;
+  }
+
+  // Ordered emission, one run index j at a time (runs of index j, in thread
+  // order, cover positions [kRun*NT*j, kRun*NT*(j+1)) in order).
+  uint32_t gt_before = 0, eq_before = 0;
+#pragma unroll
+  for (int j = 0; j < kRegSub; ++j) {
+    if (j >= nsub) break;   // uniform
+    const int p0 = kRun * (tid + NT * j);
+    uint32_t cgt = 0, ceq = 0;
+#pragma unroll
+    for (int i = 0; i < kRun; ++i) {
+      if (p0 + i < nc) {
+        cgt += key[j][i] > T;
+        ceq += key[j][i] == T;
+      }
+    }
+    uint32_t total;
+    const uint32_t ex = block_exclusive_scan<NT>((cgt << 16) | ceq, scan_scratch, &total);
+    const uint32_t my_gt = gt_before + (ex >> 16);
+    uint32_t my_eq = eq_before + (ex & 0xffffu);
+    uint32_t pos = my_gt + min(my_eq, remaining);
+#pragma unroll
+    for (int i = 0; i < kRun; ++i) {
+      if (p0 + i < nc) {
+        const uint32_t kv = key[j][i];
+        bool take = kv > T;
+        if (kv == T) {
+          take = my_eq < remaining;
+          ++my_eq;
+        }
+        if (take) {
+          if (pos < (uint32_t)kp) out[pos] = p0 + i;   // always true for consistent counts
+          ++pos;
+        }
+      }
+    }
+    gt_before += total >> 16;
+    eq_before += total & 0xffffu;
+  }
+  for (int c = tid; c < Wf; c += NT) out[kp + c] = nc + c;
+}
+
+// -------------------------------------------------------------- streamed rows
+constexpr int kNT = 256;
+constexpr int kEmitPer = 16;
 constexpr int kEmitChunk = kNT * kEmitPer;
+constexpr int kEmitStride = kNT + 4;   // LDS column stride: conflict-free writes and reads
 
 __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int b, int k, int W,
                                                         const float *__restrict__ scores,
                                                         int32_t *__restrict__ idx) {
-  __shared__ uint32_t hist[4096];
+  __shared__ uint32_t hist[2048];
   __shared__ uint32_t scan_scratch[kNT / 64 + 1];
   __shared__ uint32_t sel[2];
-  __shared__ uint32_t keys[kEmitChunk];
+  __shared__ uint32_t keys[kEmitPer * kEmitStride];
 
   const int r = blockIdx.x;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
   const int t1 = min(r * b + b, S) - 1;
   const int L = t1 + 1;
   int32_t *out = idx + (size_t)r * k;
@@ -43,49 +217,35 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int b, int k, int
     return;
   }
   const int Wf = min(W, k);
-  const int nc = L - Wf;  // candidate positions [0, nc)
-  const int kp = k - Wf;  // how many candidates to choose (nc > kp)
+  const int nc = L - Wf;
+  const int kp = k - Wf;
 
   uint32_t T = 0xffffffffu;
-  uint32_t remaining = 0;  // how many keys equal to T are taken
+  uint32_t remaining = 0;
   if (kp > 0) {
     uint32_t prefix = 0, pmask = 0;
     remaining = (uint32_t)kp;
 #pragma unroll 1
     for (int pass = 0; pass < 3; ++pass) {
-      const int shift = pass == 0 ? 20 : (pass == 1 ? 8 : 0);
-      const int nbits = pass == 2 ? 8 : 12;
-      const int nb = 1 << nbits;
+      const int shift = digit_shift(pass), nb = 1 << digit_bits(pass);
       const uint32_t dmask = (uint32_t)nb - 1u;
       for (int i = tid; i < nb; i += kNT) hist[i] = 0;
       __syncthreads();
+      uint32_t zc = 0;
       for (int i = tid; i < nc; i += kNT) {
-        const uint32_t key = float_key(row[i]);
-        if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1u);
-      }
-      __syncthreads();
-      // Thread `tid` owns bins [nb - (tid+1)*per, nb - tid*per): thread 0 the
-      // highest. An exclusive scan of the per-thread sums gives, for each
-      // thread, the number of keys in bins above its range.
-      const int per = nb / kNT;
-      const int hi = nb - tid * per;  // exclusive upper bin
-      uint32_t mine = 0;
-      for (int i = hi - per; i < hi; ++i) mine += hist[i];
-      uint32_t total;
-      const uint32_t above = block_exclusive_scan<kNT>(mine, scan_scratch, &total);
-      if (above < remaining && above + mine >= remaining) {
-        uint32_t acc = above;
-        for (int i = hi - 1; i >= hi - per; --i) {
-          const uint32_t c = hist[i];
-          if (acc + c >= remaining) {
-            sel[0] = (uint32_t)i;
-            sel[1] = remaining - acc;
-            break;
-          }
-          acc += c;
+        const uint32_t kv = float_key(row[i]);
+        if ((kv & pmask) == prefix) {
+          if (kv == kZeroKey) ++zc;
+          else atomicAdd(&hist[(kv >> shift) & dmask], 1u);
         }
       }
+      if ((kZeroKey & pmask) == prefix) {
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) zc += __shfl_xor(zc, off, 64);
+        if (lane == 0 && zc) atomicAdd(&hist[(kZeroKey >> shift) & dmask], zc);
+      }
       __syncthreads();
+      find_digit<kNT>(hist, nb, remaining, scan_scratch, sel);
       prefix |= sel[0] << shift;
       pmask |= dmask << shift;
       remaining = sel[1];
@@ -94,21 +254,22 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int b, int k, int
     T = prefix;
   }
 
-  // Ordered emission over candidates: selected = key > T, or key == T among
-  // the first `remaining` such positions.
+  // Ordered emission over candidates in chunks of kEmitChunk positions; in
+  // LDS, position q of a chunk sits at (q % kEmitPer) * kEmitStride + q / kEmitPer.
   uint32_t gt_before = 0, eq_before = 0;
   for (int base = 0; base < nc; base += kEmitChunk) {
     const int n = min(kEmitChunk, nc - base);
-    for (int i = tid; i < n; i += kNT) keys[i] = float_key(row[base + i]);
+    for (int i = tid; i < kEmitChunk; i += kNT)
+      keys[(i % kEmitPer) * kEmitStride + i / kEmitPer] = i < n ? float_key(row[base + i]) : 0u;
     __syncthreads();
     const int lo = tid * kEmitPer;
     uint32_t cgt = 0, ceq = 0;
 #pragma unroll
     for (int e = 0; e < kEmitPer; ++e) {
       if (lo + e < n) {
-        const uint32_t key = keys[lo + e];
-        cgt += key > T;
-        ceq += key == T;
+        const uint32_t kv = keys[e * kEmitStride + tid];
+        cgt += kv > T;
+        ceq += kv == T;
       }
     }
     uint32_t total;
@@ -119,18 +280,15 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int b, int k, int
 #pragma unroll
     for (int e = 0; e < kEmitPer; ++e) {
       if (lo + e < n) {
-        const uint32_t key = keys[lo + e];
-        // pos < kp always holds when the counts above are consistent; the
-        // test keeps every store inside the row regardless.
-        if (key > T) {
-          if (pos < (uint32_t)kp) out[pos] = base + lo + e;
-          ++pos;
-        } else if (key == T) {
-          if (my_eq < remaining) {
-            if (pos < (uint32_t)kp) out[pos] = base + lo + e;
-            ++pos;
-          }
+        const uint32_t kv = keys[e * kEmitStride + tid];
+        bool take = kv > T;
+        if (kv == T) {
+          take = my_eq < remaining;
           ++my_eq;
+        }
+        if (take) {
+          if (pos < (uint32_t)kp) out[pos] = base + lo + e;   // always true for consistent counts
+          ++pos;
         }
       }
     }
@@ -144,8 +302,15 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int b, int k, int
 }  // namespace
 
 hipError_t launch_topk(const Prob &p, const float *scores, int32_t *idx, hipStream_t st) {
-  hipLaunchKernelGGL(topk_rows_kernel, dim3(p.R), dim3(kNT), 0, st, p.S, p.b, p.k, p.W, scores,
-                     idx);
+  // Longest candidate range of any row: the last block's causal length minus the window.
+  const int Lmax = min(p.R * p.b, p.S);
+  const int ncmax = Lmax - min(p.W, p.k);
+  if (ncmax <= kRegCap)
+    hipLaunchKernelGGL(topk_reg_kernel, dim3(p.R), dim3(kRegNT), 0, st, p.S, p.b, p.k, p.W,
+                       scores, idx);
+  else
+    hipLaunchKernelGGL(topk_rows_kernel, dim3(p.R), dim3(kNT), 0, st, p.S, p.b, p.k, p.W,
+                       scores, idx);
   return hipGetLastError();
 }
 
