@@ -50,6 +50,12 @@ struct AttnLayout {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Wait for every outstanding memory operation of this wave. Issued once
+// before a tile loop, it tells the compiler that loads made before the loop
+// (Q fragments, the first tile) are complete, so no wait on them is placed
+// inside the loop, where it would also stall on the next tile's prefetch.
+__device__ __forceinline__ void drain_memory() { __builtin_amdgcn_s_waitcnt(0); }
+
 // Global -> registers -> LDS staging of one tile of K, V and positions.
 // pos(e) gives the position of tile entry e (0..63), or a negative value.
 template <int D, int NT, bool WANT_V>
@@ -61,23 +67,29 @@ struct KVStage {
   uint4 vreg[WANT_V ? PER : 1];
   int spos;
 
+  // All positions are resolved before any row load is issued, so the row
+  // loads of a tile go out back to back.
   template <typename POS>
   __device__ __forceinline__ void load(const uint16_t *__restrict__ k,
                                        const uint16_t *__restrict__ v, int S, int Hkv, int j,
                                        int tid, POS pos) {
+    size_t off[PER];
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int c = tid + i * NT;
-      if (c < PIECES) {
-        const int key = c / (D / 8), col = c % (D / 8);
-        int s = pos(key);
-        s = (s >= 0 && s < S) ? s : 0;
-        const size_t off = ((size_t)s * Hkv + j) * D + col * 8;
-        kreg[i] = ldg16(k + off);
-        if constexpr (WANT_V) vreg[i] = ldg16(v + off);
-      }
+      const int key = c / (D / 8), col = c % (D / 8);
+      int s = c < PIECES ? pos(key) : 0;
+      s = (s >= 0 && s < S) ? s : 0;
+      off[i] = ((size_t)s * Hkv + j) * D + col * 8;
     }
     if (tid < kAttnKT) spos = pos(tid);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if (tid + i * NT < PIECES) {
+        kreg[i] = ldg16(k + off[i]);
+        if constexpr (WANT_V) vreg[i] = ldg16(v + off[i]);
+      }
+    }
   }
 
   // Also publishes min and max of the tile's positions (wave 0 holds them).

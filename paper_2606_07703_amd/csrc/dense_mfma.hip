@@ -51,6 +51,7 @@ __global__ __launch_bounds__(kNW * 64) void dense_fwd_kernel(
   };
   stage.load(k, v, S, Hkv, j, tid, pos_of(0));
   stage.store(lds[0], tid);
+  drain_memory();
   __syncthreads();
   const bool live = row0 < nrows;
   const int wave_tmin = t0 + row0 / G;

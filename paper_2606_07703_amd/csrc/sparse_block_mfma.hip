@@ -17,6 +17,8 @@
 namespace sp {
 namespace {
 
+constexpr int kMaxSupport = 4096;   // support row cached in LDS
+
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
     int S, int Hq, int Hkv, int G, int b, int kk, float scale_log2,
@@ -27,6 +29,7 @@ __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
   constexpr int NT = NW * 64;
   __shared__ __align__(16) char lds[2][L::BUF];
   __shared__ int red_last[NW];
+  __shared__ int ir[kMaxSupport];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, c16 = lane & 15;
@@ -35,12 +38,13 @@ __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
   const int t1 = min(t0 + b, S) - 1;
   const int nrows = (t1 - t0 + 1) * G;
   const int row0 = blockIdx.z * (NW * kAttnQPW) + wave * kAttnQPW;
-  const int32_t *ir = idx + (size_t)r * kk;
 
-  // Tiles end after the last entry any query of the block can use (any order).
+  // Cache the support row; tiles end after the last entry any query of the
+  // block can use (any order).
   int last = -1;
   for (int c = tid; c < kk; c += NT) {
-    const int s = ir[c];
+    const int s = idx[(size_t)r * kk + c];
+    ir[c] = s;
     if (s >= 0 && s <= t1) last = c;
   }
 #pragma unroll
@@ -67,6 +71,7 @@ __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
     stage.load(k, v, S, Hkv, j, tid, pos_of(0));
     stage.store(lds[0], tid);
   }
+  drain_memory();
   __syncthreads();
   const bool live = row0 < nrows;
   const int wave_tmin = t0 + row0 / G;
@@ -106,7 +111,8 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
 }  // namespace
 
 bool sparse_block_mfma_supported(const Prob &p) {
-  return p.dtype == SP_DTYPE_BF16 && (p.d == 64 || p.d == 128) && p.b >= 16;
+  return p.dtype == SP_DTYPE_BF16 && (p.d == 64 || p.d == 128) && p.b >= 16 &&
+         p.k <= kMaxSupport;
 }
 
 hipError_t launch_sparse_block_mfma(const Prob &p, const void *q, const void *k, const void *v,
