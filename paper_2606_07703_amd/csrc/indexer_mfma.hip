@@ -68,6 +68,37 @@ __device__ __forceinline__ float agg2(int agg, float a, float b) {
   return agg == SP_AGG_MAX ? fmaxf(a, b) : a + b;
 }
 
+__device__ __forceinline__ float as_f(uint32_t x) { return __uint_as_float(x); }
+__device__ __forceinline__ uint32_t as_u(float x) { return __float_as_uint(x); }
+
+// Reduce-scatter across the four 16-lane groups of a wave. Every lane holds
+// one partial per column tile; afterwards lane (g, c) holds the reduction over
+// the four groups of column tile owned_ct(g) at column c. Two half-wave swaps
+// and one row swap (gfx950 v_permlane32_swap / v_permlane16_swap) replace the
+// eight cross-lane shuffles a per-tile butterfly would take.
+template <int NCT>
+__device__ __forceinline__ int owned_ct(int g) {
+  return NCT == 4 ? ((g & 1) << 1) | (g >> 1) : g >> 1;
+}
+
+template <class Op>
+__device__ __forceinline__ float reduce_scatter(const float (&v)[4], Op op) {
+  const auto a = __builtin_amdgcn_permlane32_swap(as_u(v[0]), as_u(v[1]), false, false);
+  const auto b = __builtin_amdgcn_permlane32_swap(as_u(v[2]), as_u(v[3]), false, false);
+  const float m01 = op(as_f(a[0]), as_f(a[1]));   // rows 0,1: tile 0; rows 2,3: tile 1
+  const float m23 = op(as_f(b[0]), as_f(b[1]));   // rows 0,1: tile 2; rows 2,3: tile 3
+  const auto c = __builtin_amdgcn_permlane16_swap(as_u(m01), as_u(m23), false, false);
+  return op(as_f(c[0]), as_f(c[1]));
+}
+
+template <class Op>
+__device__ __forceinline__ float reduce_scatter(const float (&v)[2], Op op) {
+  const auto a = __builtin_amdgcn_permlane32_swap(as_u(v[0]), as_u(v[1]), false, false);
+  const float m = op(as_f(a[0]), as_f(a[1]));     // rows 0,1: tile 0; rows 2,3: tile 1
+  const auto c = __builtin_amdgcn_permlane16_swap(as_u(m), as_u(m), false, false);
+  return op(as_f(c[0]), as_f(c[1]));
+}
+
 // MAXPOS: aggregation is max and the scale is non-negative, so scale and
 // ReLU commute with the max: rows are reduced on raw MFMA outputs and only
 // the reduced value is scaled; tiles entirely below a wave's first query
@@ -80,6 +111,7 @@ __global__ __launch_bounds__(512) void indexer_block_kernel(int S, int agg, int 
                                                             float *__restrict__ Y) {
   constexpr int NT = 512, NW = 8;
   constexpr int KT = Tile<DI>::KT, RB = Tile<DI>::RB, KS = Tile<DI>::KS;
+  constexpr int NCT = KT / 16;
   constexpr int QG = NW * kQW;
   __shared__ __align__(16) char lds[2][Tile<DI>::BYTES];
   __shared__ float red[NW / 2][KT];
@@ -94,6 +126,9 @@ __global__ __launch_bounds__(512) void indexer_block_kernel(int S, int agg, int 
   const int ntiles = (k_end - k_begin + KT - 1) / KT;
   const int qw0 = q0 + wave * kQW;
   const int qw_last = min(qw0 + kQW, S) - 1;  // < qw0 when the wave is past the end
+  // key column this lane holds after the reduce-scatter (relative to the tile)
+  const int my_col = owned_ct<NCT>(g) * 16 + c16;
+  const bool col_writer = NCT == 4 || (g & 1) == 0;
 
   bf16x8 a[4][KS];
 #pragma unroll
@@ -110,23 +145,26 @@ __global__ __launch_bounds__(512) void indexer_block_kernel(int S, int agg, int 
   __syncthreads();
 
   const float neutral = agg == SP_AGG_MAX ? -INFINITY : 0.f;
+  auto op = [agg](float x, float y) { return MAXPOS ? fmaxf(x, y) : agg2(agg, x, y); };
+  constexpr int BPW = BQ >= kQW ? 1 : kQW / BQ;   // blocks per wave
+  constexpr int RPB = BQ >= kQW ? 4 : BQ / 16;    // row tiles per block
   for (int it = 0; it < ntiles; ++it) {
     const int kt0 = k_begin + it * KT;
     const bool more = it + 1 < ntiles;
     if (more) stage.load(ki, S, kt0 + KT, tid);
     const char *cur = lds[it & 1];
     const bool active = kt0 <= qw_last;
-    // reduced[ct][blk]: aggregate over the wave's queries of block blk for
-    // the 16 keys of column tile ct (valid in every lane after the shuffles)
-    constexpr int BPW = BQ >= kQW ? 1 : kQW / BQ;   // blocks per wave
-    constexpr int RPB = BQ >= kQW ? 4 : BQ / 16;    // row tiles per block
-    float reduced[KT / 16][BPW];
+    // full: every (query, key) pair of the wave and tile is causal and valid
+    const bool full = kt0 + KT - 1 <= qw0 && qw0 + kQW - 1 <= qw_last;
+    // out[bb]: aggregate over the queries of block bb, for key column my_col
+    float out[BPW];
 #pragma unroll
-    for (int ct = 0; ct < KT / 16; ++ct) {
-      const int s = kt0 + ct * 16 + c16;
+    for (int bb = 0; bb < BPW; ++bb) out[bb] = neutral;
+    if (active) {
+      float part[BPW][NCT];
 #pragma unroll
-      for (int bb = 0; bb < BPW; ++bb) reduced[ct][bb] = neutral;
-      if (active) {
+      for (int ct = 0; ct < NCT; ++ct) {
+        const int s = kt0 + ct * 16 + c16;
         f32x4 acc[4];
 #pragma unroll
         for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -136,82 +174,57 @@ __global__ __launch_bounds__(512) void indexer_block_kernel(int S, int agg, int 
 #pragma unroll
           for (int rt = 0; rt < 4; ++rt) acc[rt] = mfma16(a[rt][ks], b, acc[rt]);
         }
-        if constexpr (MAXPOS) {
-          const bool full = kt0 + KT - 1 <= qw0 && qw0 + kQW - 1 <= qw_last;
 #pragma unroll
-          for (int rt = 0; rt < 4; ++rt) {
-            float m;
-            if (full) {
-              m = fmaxf(fmaxf(acc[rt][0], acc[rt][1]), fmaxf(acc[rt][2], acc[rt][3]));
-            } else {
-              m = -INFINITY;
+        for (int bb = 0; bb < BPW; ++bb) part[bb][ct] = neutral;
 #pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                const int t = qw0 + rt * 16 + g * 4 + r;
-                m = fmaxf(m, (t <= qw_last && s <= t) ? acc[rt][r] : -INFINITY);
-              }
+        for (int rt = 0; rt < 4; ++rt) {
+          float x[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            x[r] = acc[rt][r];
+            if constexpr (!MAXPOS) {
+              x[r] *= scale;
+              if (relu) x[r] = fmaxf(x[r], 0.f);
             }
-            reduced[ct][rt / RPB] = fmaxf(reduced[ct][rt / RPB], m);
           }
-#pragma unroll
-          for (int bb = 0; bb < BPW; ++bb) {
-            float m = reduced[ct][bb];
-            m = fmaxf(m, __shfl_xor(m, 16, 64));
-            m = fmaxf(m, __shfl_xor(m, 32, 64));
-            m *= scale;
-            if (relu) m = fmaxf(m, 0.f);   // -inf (no causal row) becomes 0; never stored
-            reduced[ct][bb] = m;
-          }
-        } else {
-#pragma unroll
-          for (int rt = 0; rt < 4; ++rt) {
-            float m = neutral;
+          if (!full) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const int t = qw0 + rt * 16 + g * 4 + r;
-              float x = acc[rt][r] * scale;
-              if (relu) x = x > 0.f ? x : 0.f;
-              m = agg2(agg, m, (t <= qw_last && s <= t) ? x : neutral);
+              if (!(t <= qw_last && s <= t)) x[r] = neutral;
             }
-            reduced[ct][rt / RPB] = agg2(agg, reduced[ct][rt / RPB], m);
           }
-#pragma unroll
-          for (int bb = 0; bb < BPW; ++bb) {
-            float m = reduced[ct][bb];
-            m = agg2(agg, m, __shfl_xor(m, 16, 64));
-            m = agg2(agg, m, __shfl_xor(m, 32, 64));
-            reduced[ct][bb] = m;
-          }
+          const float m = op(op(x[0], x[1]), op(x[2], x[3]));
+          part[rt / RPB][ct] = op(part[rt / RPB][ct], m);
         }
       }
+#pragma unroll
+      for (int bb = 0; bb < BPW; ++bb) {
+        float m = reduce_scatter(part[bb], op);
+        if constexpr (MAXPOS) {
+          m *= scale;
+          if (relu) m = fmaxf(m, 0.f);   // -inf (no causal row) becomes 0; never stored
+        }
+        out[bb] = m;
+      }
     }
+    const int s = kt0 + my_col;
     if constexpr (BQ <= kQW) {
 #pragma unroll
-      for (int ct = 0; ct < KT / 16; ++ct) {
-        const int s = kt0 + ct * 16 + c16;
-#pragma unroll
-        for (int bb = 0; bb < BPW; ++bb) {
-          const int tb0 = qw0 + bb * BQ;                  // first query of the block
-          const int tb1 = min(tb0 + BQ, S) - 1;
-          if (g == 0 && tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = reduced[ct][bb];
-        }
+      for (int bb = 0; bb < BPW; ++bb) {
+        const int tb0 = qw0 + bb * BQ;                  // first query of the block
+        const int tb1 = min(tb0 + BQ, S) - 1;
+        if (col_writer && tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = out[bb];
       }
     } else {
       // BQ = 128: waves 2i and 2i+1 hold the two halves of one block.
-      if ((wave & 1) && g == 0) {
-#pragma unroll
-        for (int ct = 0; ct < KT / 16; ++ct) red[wave >> 1][ct * 16 + c16] = reduced[ct][0];
-      }
+      if (wave & 1) red[wave >> 1][my_col] = out[0];
       __syncthreads();
-      if (!(wave & 1) && g == 0) {
+      if (!(wave & 1)) {
         const int tb0 = qw0;
         const int tb1 = min(tb0 + BQ, S) - 1;
-#pragma unroll
-        for (int ct = 0; ct < KT / 16; ++ct) {
-          const int s = kt0 + ct * 16 + c16;
-          const float m = agg2(agg, reduced[ct][0], red[wave >> 1][ct * 16 + c16]);
-          if (tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = m;
-        }
+        const float m = op(out[0], red[wave >> 1][my_col]);
+        if (col_writer && tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = m;
       }
     }
     if (more) stage.store(lds[(it + 1) & 1], tid);
