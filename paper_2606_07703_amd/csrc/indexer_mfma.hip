@@ -25,7 +25,8 @@ namespace sp {
 namespace {
 
 constexpr int kQW = 64;     // queries per wave
-constexpr int kKC = 1024;   // keys per workgroup chunk
+constexpr int kKC = 1024;   // keys per workgroup chunk (rows kernel)
+constexpr int kXcds = 8;    // XCDs of the chip; workgroup i runs on XCD i % 8
 
 template <int DI>
 struct Tile {
@@ -103,32 +104,104 @@ __device__ __forceinline__ float reduce_scatter(const float (&v)[2], Op op) {
 // ReLU commute with the max: rows are reduced on raw MFMA outputs and only
 // the reduced value is scaled; tiles entirely below a wave's first query
 // skip the causal test.
-template <int DI, int BQ, bool MAXPOS>
-__global__ __launch_bounds__(512) void indexer_block_kernel(int S, int agg, int relu,
-                                                            float scale,
-                                                            const uint16_t *__restrict__ qi,
-                                                            const uint16_t *__restrict__ ki,
-                                                            float *__restrict__ Y) {
-  constexpr int NT = 512, NW = 8;
-  constexpr int KT = Tile<DI>::KT, RB = Tile<DI>::RB, KS = Tile<DI>::KS;
-  constexpr int NCT = KT / 16;
+// Work items of the block kernel are the causal (query group, key chunk)
+// pairs: chunk kc (keys kc*KC ..) meets query groups qg >= kc*KC/QG. Items are
+// numbered by chunk, so neighbouring items share their key chunk, and
+// workgroup i (which the hardware places on XCD i % 8) takes item
+// xcd_range_start + i / 8: each XCD walks a contiguous run of items and its L2
+// sees each key chunk once for several query groups.
+template <int QG, int KC>
+__device__ __forceinline__ void decode_item(int i, int n_items, int S, int &qg, int &kc) {
+  const int x = i % kXcds, j = i / kXcds;
+  const int lin = x * (n_items / kXcds) + min(x, n_items % kXcds) + j;
+  const int nqg = (S + QG - 1) / QG;
+  int c = 0, base = 0;
+  for (;;) {
+    const int cnt = nqg - c * KC / QG;
+    if (lin < base + cnt) break;
+    base += cnt;
+    ++c;
+  }
+  kc = c;
+  qg = c * KC / QG + (lin - base);
+}
+
+template <int QG, int KC>
+int count_items(int S) {
+  const int nqg = (S + QG - 1) / QG, nkc = (S + KC - 1) / KC;
+  int n = 0;
+  for (int c = 0; c < nkc; ++c) n += nqg - c * KC / QG;
+  return n;
+}
+
+// Key tiles of the block kernel: NSUB sub-tiles of 64 keys, staged
+// PD tiles ahead through registers into a ring of PD + 1 LDS buffers.
+template <int DI>
+struct BlockTile {
+  static constexpr int NSUB = DI <= 128 ? 2 : 1;
+  static constexpr int PD = 1;
+  static constexpr int KT = 64 * NSUB;
+  static constexpr int RB = DI * 2 + 16;
+  static constexpr int BYTES = KT * RB;
+  static constexpr int NB = PD + 1;
+};
+
+template <int DI, int KT, int RB, int NT>
+struct KeyStageT {
+  static constexpr int CHUNKS = KT * DI / 8;
+  static constexpr int PER = (CHUNKS + NT - 1) / NT;
+  uint4 reg[PER];
+  __device__ __forceinline__ void load(const uint16_t *__restrict__ ki, int S, int k0, int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * NT;
+      if (c < CHUNKS) {
+        const int row = c / (DI / 8), col = c % (DI / 8);
+        const int s = min(k0 + row, S - 1);
+        reg[i] = ldg16(ki + (size_t)s * DI + col * 8);
+      }
+    }
+  }
+  __device__ __forceinline__ void store(char *lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * NT;
+      if (c < CHUNKS) {
+        const int row = c / (DI / 8), col = c % (DI / 8);
+        sts16(lds + row * RB + col * 16, reg[i]);
+      }
+    }
+  }
+};
+
+template <int DI, int BQ, bool MAXPOS, int NW, int KC>
+__global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_items, int agg,
+                                                                int relu, float scale,
+                                                                const uint16_t *__restrict__ qi,
+                                                                const uint16_t *__restrict__ ki,
+                                                                float *__restrict__ Y) {
+  using T = BlockTile<DI>;
+  constexpr int NT = NW * 64;
+  constexpr int KT = T::KT, RB = T::RB, KS = DI / 32, NSUB = T::NSUB, PD = T::PD, NB = T::NB;
   constexpr int QG = NW * kQW;
-  __shared__ __align__(16) char lds[2][Tile<DI>::BYTES];
+  static_assert(KC % QG == 0 || QG % KC == 0, "chunk and query group sizes must nest");
+  static_assert(KC % KT == 0, "chunks hold whole tiles");
+  __shared__ __align__(16) char lds[NB][T::BYTES];
   __shared__ float red[NW / 2][KT];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, c16 = lane & 15;
-  const int q0 = blockIdx.x * QG;
-  const int k_begin = blockIdx.y * kKC;
+  int qg, kc;
+  decode_item<QG, KC>(blockIdx.x, n_items, S, qg, kc);
+  const int q0 = qg * QG;
+  const int k_begin = kc * KC;
   const int q_last = min(q0 + QG, S) - 1;
-  if (k_begin > q_last) return;
-  const int k_end = min(k_begin + kKC, q_last + 1);
+  const int k_end = min(k_begin + KC, q_last + 1);
   const int ntiles = (k_end - k_begin + KT - 1) / KT;
   const int qw0 = q0 + wave * kQW;
   const int qw_last = min(qw0 + kQW, S) - 1;  // < qw0 when the wave is past the end
-  // key column this lane holds after the reduce-scatter (relative to the tile)
-  const int my_col = owned_ct<NCT>(g) * 16 + c16;
-  const bool col_writer = NCT == 4 || (g & 1) == 0;
+  // key column (within a 64-key sub-tile) this lane holds after the reduce-scatter
+  const int my_col = owned_ct<4>(g) * 16 + c16;
 
   bf16x8 a[4][KS];
 #pragma unroll
@@ -139,96 +212,131 @@ __global__ __launch_bounds__(512) void indexer_block_kernel(int S, int agg, int 
       a[rt][ks] = as_bf16x8(ldg16(qi + (size_t)row * DI + ks * 32 + g * 8));
   }
 
-  KeyStage<DI, NT> stage;
-  stage.load(ki, S, k_begin, tid);
-  stage.store(lds[0], tid);
+  KeyStageT<DI, KT, RB, NT> stage[PD];
+#pragma unroll
+  for (int j = 0; j < PD; ++j)
+    if (j < ntiles) stage[j].load(ki, S, k_begin + j * KT, tid);
+  stage[0].store(lds[0], tid);
   __syncthreads();
 
   const float neutral = agg == SP_AGG_MAX ? -INFINITY : 0.f;
   auto op = [agg](float x, float y) { return MAXPOS ? fmaxf(x, y) : agg2(agg, x, y); };
   constexpr int BPW = BQ >= kQW ? 1 : kQW / BQ;   // blocks per wave
   constexpr int RPB = BQ >= kQW ? 4 : BQ / 16;    // row tiles per block
-  for (int it = 0; it < ntiles; ++it) {
-    const int kt0 = k_begin + it * KT;
-    const bool more = it + 1 < ntiles;
-    if (more) stage.load(ki, S, kt0 + KT, tid);
-    const char *cur = lds[it & 1];
-    const bool active = kt0 <= qw_last;
-    // full: every (query, key) pair of the wave and tile is causal and valid
-    const bool full = kt0 + KT - 1 <= qw0 && qw0 + kQW - 1 <= qw_last;
-    // out[bb]: aggregate over the queries of block bb, for key column my_col
-    float out[BPW];
+
+  // One 64-key sub-tile: scores of the wave's 64 queries, masked unless FULL
+  // (every pair causal and valid), reduced per selection block; returns the
+  // reduction for key column my_col in out[bb].
+  auto subtile = [&](const char *cur, int sb, int ks0, float (&out)[BPW], auto full_) {
+    constexpr bool FULL = decltype(full_)::value;
+    float part[BPW][4];
 #pragma unroll
-    for (int bb = 0; bb < BPW; ++bb) out[bb] = neutral;
-    if (active) {
-      float part[BPW][NCT];
+    for (int ct = 0; ct < 4; ++ct) {
+      const int s = ks0 + ct * 16 + c16;
+      const char *krow = cur + (sb * 64 + ct * 16 + c16) * RB + g * 16;
+      f32x4 acc[4];
 #pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) {
-        const int s = kt0 + ct * 16 + c16;
-        f32x4 acc[4];
+      for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 b = as_bf16x8(lds16(krow + ks * 64));
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 b = as_bf16x8(lds16(cur + (ct * 16 + c16) * RB + ks * 64 + g * 16));
-#pragma unroll
-          for (int rt = 0; rt < 4; ++rt) acc[rt] = mfma16(a[rt][ks], b, acc[rt]);
-        }
-#pragma unroll
-        for (int bb = 0; bb < BPW; ++bb) part[bb][ct] = neutral;
-#pragma unroll
-        for (int rt = 0; rt < 4; ++rt) {
-          float x[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            x[r] = acc[rt][r];
-            if constexpr (!MAXPOS) {
-              x[r] *= scale;
-              if (relu) x[r] = fmaxf(x[r], 0.f);
-            }
-          }
-          if (!full) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int t = qw0 + rt * 16 + g * 4 + r;
-              if (!(t <= qw_last && s <= t)) x[r] = neutral;
-            }
-          }
-          const float m = op(op(x[0], x[1]), op(x[2], x[3]));
-          part[rt / RPB][ct] = op(part[rt / RPB][ct], m);
-        }
+        for (int rt = 0; rt < 4; ++rt) acc[rt] = mfma16(a[rt][ks], b, acc[rt]);
       }
 #pragma unroll
-      for (int bb = 0; bb < BPW; ++bb) {
-        float m = reduce_scatter(part[bb], op);
-        if constexpr (MAXPOS) {
-          m *= scale;
-          if (relu) m = fmaxf(m, 0.f);   // -inf (no causal row) becomes 0; never stored
+      for (int bb = 0; bb < BPW; ++bb) part[bb][ct] = neutral;
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        float x[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          x[r] = acc[rt][r];
+          if constexpr (!MAXPOS) {
+            x[r] *= scale;
+            if (relu) x[r] = fmaxf(x[r], 0.f);
+          }
+          if constexpr (!FULL) {
+            const int t = qw0 + rt * 16 + g * 4 + r;
+            if (!(t <= qw_last && s <= t)) x[r] = neutral;
+          }
         }
-        out[bb] = m;
+        const float m = op(op(x[0], x[1]), op(x[2], x[3]));
+        part[rt / RPB][ct] = op(part[rt / RPB][ct], m);
       }
     }
-    const int s = kt0 + my_col;
+#pragma unroll
+    for (int bb = 0; bb < BPW; ++bb) {
+      float m = reduce_scatter(part[bb], op);
+      if constexpr (MAXPOS) {
+        m *= scale;
+        if (relu) m = fmaxf(m, 0.f);   // -inf (no causal row) becomes 0; never stored
+      }
+      out[bb] = m;
+    }
+  };
+
+  auto tile = [&](int it, auto j_) {
+    constexpr int j = decltype(j_)::value;   // it % PD
+    const int kt0 = k_begin + it * KT;
+    if (it + PD < ntiles) stage[j].load(ki, S, kt0 + PD * KT, tid);
+    const char *cur = lds[it % NB];
+    // out[sb][bb]: aggregate over the queries of block bb, key kt0 + 64 sb + my_col
+    float out[NSUB][BPW];
+    // (DI = 256 keeps one code path: its 128 query registers leave no room
+    // for two instantiations of the sub-tile)
+    if (DI <= 128 && kt0 + KT - 1 <= qw0 && qw0 + kQW - 1 <= qw_last) {
+      // whole tile below the wave's first query: no masks, no branches, so
+      // the sub-tiles' MFMAs and reductions interleave
+      if constexpr (DI <= 128) {
+#pragma unroll
+        for (int sb = 0; sb < NSUB; ++sb)
+          subtile(cur, sb, kt0 + sb * 64, out[sb], std::true_type{});
+      }
+    } else {
+#pragma unroll
+      for (int sb = 0; sb < NSUB; ++sb) {
+        const int ks0 = kt0 + sb * 64;
+#pragma unroll
+        for (int bb = 0; bb < BPW; ++bb) out[sb][bb] = neutral;
+        if (ks0 <= qw_last) subtile(cur, sb, ks0, out[sb], std::false_type{});
+      }
+    }
     if constexpr (BQ <= kQW) {
 #pragma unroll
-      for (int bb = 0; bb < BPW; ++bb) {
-        const int tb0 = qw0 + bb * BQ;                  // first query of the block
-        const int tb1 = min(tb0 + BQ, S) - 1;
-        if (col_writer && tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = out[bb];
+      for (int sb = 0; sb < NSUB; ++sb) {
+        const int s = kt0 + sb * 64 + my_col;
+#pragma unroll
+        for (int bb = 0; bb < BPW; ++bb) {
+          const int tb0 = qw0 + bb * BQ;                  // first query of the block
+          const int tb1 = min(tb0 + BQ, S) - 1;
+          if (tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = out[sb][bb];
+        }
       }
     } else {
       // BQ = 128: waves 2i and 2i+1 hold the two halves of one block.
-      if (wave & 1) red[wave >> 1][my_col] = out[0];
+      if (wave & 1) {
+#pragma unroll
+        for (int sb = 0; sb < NSUB; ++sb) red[wave >> 1][sb * 64 + my_col] = out[sb][0];
+      }
       __syncthreads();
       if (!(wave & 1)) {
         const int tb0 = qw0;
         const int tb1 = min(tb0 + BQ, S) - 1;
-        const float m = op(out[0], red[wave >> 1][my_col]);
-        if (col_writer && tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = m;
+#pragma unroll
+        for (int sb = 0; sb < NSUB; ++sb) {
+          const int s = kt0 + sb * 64 + my_col;
+          const float m = op(out[sb][0], red[wave >> 1][sb * 64 + my_col]);
+          if (tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = m;
+        }
       }
     }
-    if (more) stage.store(lds[(it + 1) & 1], tid);
+    if (it + 1 < ntiles) stage[(j + 1) % PD].store(lds[(it + 1) % NB], tid);
     __syncthreads();
+  };
+  for (int it0 = 0; it0 < ntiles; it0 += PD) {
+    static_for<0, PD>([&](auto j_) {
+      if (it0 + decltype(j_)::value < ntiles) tile(it0 + decltype(j_)::value, j_);
+    });
   }
 }
 
@@ -331,15 +439,18 @@ hipError_t launch_di(const Prob &p, const void *qi, const void *ki, float *score
                          p.iscale, q, k, scores);
     return hipGetLastError();
   }
-  dim3 grid((p.S + 511) / 512, (p.S + kKC - 1) / kKC);
+  constexpr int NW = 8, KC = 1024;
+  const int n_items = count_items<NW * kQW, KC>(p.S);
   const bool maxpos = p.agg == SP_AGG_MAX && p.iscale >= 0.f;
 #define SP_BLK(BQ)                                                                           \
   if (maxpos)                                                                                \
-    hipLaunchKernelGGL((indexer_block_kernel<DI, BQ, true>), grid, dim3(512), 0, st, p.S,    \
-                       p.agg, p.relu, p.iscale, q, k, scores);                               \
+    hipLaunchKernelGGL((indexer_block_kernel<DI, BQ, true, NW, KC>), dim3(n_items),          \
+                       dim3(NW * 64), 0, st, p.S, n_items, p.agg, p.relu, p.iscale, q, k,    \
+                       scores);                                                              \
   else                                                                                       \
-    hipLaunchKernelGGL((indexer_block_kernel<DI, BQ, false>), grid, dim3(512), 0, st, p.S,   \
-                       p.agg, p.relu, p.iscale, q, k, scores)
+    hipLaunchKernelGGL((indexer_block_kernel<DI, BQ, false, NW, KC>), dim3(n_items),         \
+                       dim3(NW * 64), 0, st, p.S, n_items, p.agg, p.relu, p.iscale, q, k,    \
+                       scores)
   switch (p.b) {
     case 16: SP_BLK(16); break;
     case 32: SP_BLK(32); break;
