@@ -30,6 +30,9 @@ sys.path.insert(0, ROOT)
 import numpy as np  # noqa: E402
 import torch  # noqa: E402
 
+from paper_2606_07703_amd.traffic import stage_traffic  # noqa: E402
+
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "traffic_headline_32k.md")
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 FP32_VALU_PEAK_TFLOPS = 157.3
@@ -48,6 +51,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-units", type=int, default=256,
                     help="selection blocks the CPU oracle times (bounded sample)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after timing, run one device copy of this size (the calibration "
+                         "kernel for rocprofv3 FETCH_SIZE/WRITE_SIZE runs)")
     return ap.parse_args()
 
 
@@ -137,6 +143,12 @@ def main():
     med = {n: float(np.median(v)) for n, v in per_stage.items()}
     mean = {n: float(np.mean(v)) for n, v in per_stage.items()}
     print("[bench] timed steps done", file=sys.stderr, flush=True)
+    if args.copy_mib > 0:
+        src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ---------------------------------------------------------- algorithmic work
     C = causal_pairs(S)
@@ -179,6 +191,9 @@ def main():
         if nbytes is not None:
             ent["gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
             ent["frac_hbm"] = round(ent["gbs"] / HBM_PEAK_GBS, 4)
+        tb = stage_traffic(TRAFFIC_SUMMARY, name)
+        if tb is not None:
+            ent["traffic_gb"] = round(tb / 1e9, 3)
         kernels[name] = ent
 
     block_ms = sum(med[n] for n in ("block64.indexer_scores", "block64.topk", "block64.sparse_attn"))
@@ -197,7 +212,9 @@ def main():
         roof = {"bound": "hbm", "achieved": round(nbytes / (ms_dom * 1e-3) / 1e9, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = None
+    # HBM bytes per launch from the committed rocprofv3 counter runs, only while
+    # the kernel's sources are unchanged since they were taken
+    roof["traffic"] = stage_traffic(TRAFFIC_SUMMARY, dom)
     roof["kernel"] = dom
     roof["launch_ms"] = round(ms_dom, 4)
 

@@ -1,0 +1,198 @@
+"""HBM traffic per kernel launch from rocprofv3 counter runs.
+
+Two `rocprofv3 --pmc` runs of the same bench command, one collecting
+FETCH_SIZE and one WRITE_SIZE (KiB per dispatch, summed over the L2
+channels), give the bytes each launch moves between L2 and memory. Each
+counter is scaled by what it reads for a plain device copy of known size run
+in the same process (`bench.py --copy-mib N`): factor = true bytes / counted
+bytes, so a read of B bytes reports as B.
+
+The summary is a Markdown file under profiles/ holding, per bench stage, the
+raw counts, the scaled bytes per launch, and a digest of the sources the
+stage's kernel is built from. bench.py reports a stage's traffic only while
+that digest still matches the tree (a changed kernel reports null).
+
+    python -m paper_2606_07703_amd.traffic \\
+        --fetch DIR --write DIR --copy-mib 1024 --out profiles/traffic_....md \\
+        --cmd-fetch "..." --cmd-write "..."
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import os
+import re
+from typing import Dict, List, Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+
+# bench stage -> HIP source of the kernel it launches
+STAGE_KERNEL_FILE = {
+    "block64.indexer_scores": "indexer_mfma.hip",
+    "block64.topk": "topk.hip",
+    "block64.sparse_attn": "sparse_block_mfma.hip",
+    "perquery.indexer_scores": "indexer_mfma.hip",
+    "perquery.topk": "topk.hip",
+    "perquery.sparse_attn": "attn_rowwise.hip",
+    "dense.attn": "dense_mfma.hip",
+    "oracle.normalisers": "dense_mfma.hip",
+    "oracle.mass": "mass_mfma.hip",
+    "oracle.topk": "topk.hip",
+    "oracle.sparse_attn": "attn_rowwise.hip",
+}
+STAGES = list(STAGE_KERNEL_FILE)
+
+# kernels of the library (everything else in a trace is torch or the runtime)
+LIB_KERNEL_RE = re.compile(r"sp::|_ZN2sp")
+COPY_KERNEL_RE = re.compile(r"copy|elementwise", re.I)
+
+
+def kernel_sources(hip_file: str) -> List[str]:
+    """The kernel's source and every local header it includes (recursively),
+    plus the dispatch layer and the build flags, as paths relative to ROOT."""
+    seen: List[str] = []
+    todo = [os.path.join(CSRC, hip_file)]
+    while todo:
+        f = todo.pop()
+        if f in seen or not os.path.exists(f):
+            continue
+        seen.append(f)
+        for m in re.finditer(r'^#include "([^"]+)"', open(f).read(), re.M):
+            todo.append(os.path.join(os.path.dirname(f), m.group(1)))
+    seen += [os.path.join(CSRC, "api.cpp"), os.path.join(PKG, "build.py")]
+    return sorted(os.path.relpath(f, ROOT) for f in seen)
+
+
+def sources_digest(files: List[str]) -> str:
+    h = hashlib.sha256()
+    for f in files:
+        h.update(f.encode())
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def read_dispatches(run_dir: str, counter: str) -> List[Dict]:
+    """[{id, name, value}] in dispatch order for one counter (KiB)."""
+    paths = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not paths:
+        raise FileNotFoundError(f"no counter_collection.csv under {run_dir}")
+    per: Dict[int, Dict] = {}
+    for p in paths:
+        for r in csv.DictReader(open(p)):
+            if r["Counter_Name"] != counter:
+                continue
+            did = int(r["Dispatch_Id"])
+            e = per.setdefault(did, {"id": did, "name": r["Kernel_Name"], "value": 0.0})
+            e["value"] += float(r["Counter_Value"])
+    return [per[k] for k in sorted(per)]
+
+
+def summarize(fetch_dir: str, write_dir: str, copy_bytes: int) -> Dict:
+    out = {"copy_bytes": copy_bytes, "stages": {}}
+    for counter, run_dir, key in (("FETCH_SIZE", fetch_dir, "fetch"),
+                                  ("WRITE_SIZE", write_dir, "write")):
+        ds = read_dispatches(run_dir, counter)
+        lib = [d for d in ds if LIB_KERNEL_RE.search(d["name"])]
+        copies = [d for d in ds if not LIB_KERNEL_RE.search(d["name"])
+                  and COPY_KERNEL_RE.search(d["name"])]
+        if len(lib) % len(STAGES):
+            raise ValueError(f"{counter}: {len(lib)} library dispatches is not a whole number "
+                             f"of {len(STAGES)}-stage steps")
+        if not copies:
+            raise ValueError(f"{counter}: no copy dispatch for calibration")
+        # the calibration copy is the largest copy dispatch
+        cal_kib = max(d["value"] for d in copies)
+        factor = copy_bytes / (cal_kib * 1024.0)
+        out[f"{key}_copy_kib"] = cal_kib
+        out[f"{key}_factor"] = factor
+        nsteps = len(lib) // len(STAGES)
+        for i, st in enumerate(STAGES):
+            vals = [lib[s * len(STAGES) + i]["value"] for s in range(nsteps)]
+            kib = sum(vals) / len(vals)
+            e = out["stages"].setdefault(st, {"kernel": _short(lib[i]["name"])})
+            e[f"{key}_kib"] = kib
+            e[f"{key}_bytes"] = kib * 1024.0 * factor
+    for st, e in out["stages"].items():
+        e["traffic_bytes"] = e["fetch_bytes"] + e["write_bytes"]
+        files = kernel_sources(STAGE_KERNEL_FILE[st])
+        e["sources"] = files
+        e["digest"] = sources_digest(files)
+    return out
+
+
+def _short(name: str) -> str:
+    m = re.search(r"(\w+_kernel)(<[^()]*>)?", name)
+    return (m.group(1) + (m.group(2) or "")) if m else name[:80]
+
+
+def write_md(path: str, s: Dict, cmd_fetch: str, cmd_write: str, parse_cmd: str) -> None:
+    L = ["# HBM traffic per launch: headline 32K workload, every bench stage", "",
+         "L2 <-> memory bytes per kernel launch from two rocprofv3 counter runs of one",
+         "bench step (FETCH_SIZE, then WRITE_SIZE), each scaled by the same counter on a",
+         f"device copy of {s['copy_bytes']} bytes run in the same process.", "",
+         "Commands (repository root, one MI355X):", "",
+         "    " + cmd_fetch, "    " + cmd_write, "    " + parse_cmd, "",
+         f"Calibration: FETCH_SIZE read {s['fetch_copy_kib']:.1f} KiB for the copy "
+         f"(factor {s['fetch_factor']:.4f}); WRITE_SIZE read {s['write_copy_kib']:.1f} KiB "
+         f"(factor {s['write_factor']:.4f}).", "",
+         "| stage | kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | read bytes | written bytes "
+         "| traffic bytes | digest |",
+         "|---|---|---:|---:|---:|---:|---:|---|"]
+    for st in STAGES:
+        e = s["stages"][st]
+        L.append(f"| {st} | `{e['kernel']}` | {e['fetch_kib']:.1f} | {e['write_kib']:.1f} | "
+                 f"{e['fetch_bytes']:.4g} | {e['write_bytes']:.4g} | {e['traffic_bytes']:.4g} "
+                 f"| {e['digest']} |")
+    L += ["", "Digest = first 16 hex digits of sha256 over these sources (path, then bytes):", ""]
+    for st in STAGES:
+        L.append(f"- {st}: " + ", ".join(s["stages"][st]["sources"]))
+    L.append("")
+    L.append("<!-- machine-readable: stage traffic_bytes digest -->")
+    for st in STAGES:
+        e = s["stages"][st]
+        L.append(f"<!-- traffic {st} {e['traffic_bytes']:.6e} {e['digest']} -->")
+    open(path, "w").write("\n".join(L) + "\n")
+
+
+def load_traffic(path: str) -> Dict[str, Dict]:
+    """{stage: {"bytes": float, "digest": str, "current": bool}} from a summary file."""
+    out: Dict[str, Dict] = {}
+    if not os.path.exists(path):
+        return out
+    for m in re.finditer(r"<!-- traffic (\S+) (\S+) (\S+) -->", open(path).read()):
+        st, nbytes, dig = m.group(1), float(m.group(2)), m.group(3)
+        cur = st in STAGE_KERNEL_FILE and \
+            sources_digest(kernel_sources(STAGE_KERNEL_FILE[st])) == dig
+        out[st] = {"bytes": nbytes, "digest": dig, "current": cur}
+    return out
+
+
+def stage_traffic(path: str, stage: str) -> Optional[float]:
+    e = load_traffic(path).get(stage)
+    return e["bytes"] if e and e["current"] else None
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--fetch", required=True, help="rocprofv3 output dir of the FETCH_SIZE run")
+    ap.add_argument("--write", required=True, help="rocprofv3 output dir of the WRITE_SIZE run")
+    ap.add_argument("--copy-mib", type=int, required=True)
+    ap.add_argument("--out", required=True)
+    ap.add_argument("--cmd-fetch", required=True)
+    ap.add_argument("--cmd-write", required=True)
+    a = ap.parse_args(argv)
+    s = summarize(a.fetch, a.write, a.copy_mib << 20)
+    parse_cmd = (f"python3 -m paper_2606_07703_amd.traffic --fetch {a.fetch} --write {a.write} "
+                 f"--copy-mib {a.copy_mib} --out {a.out} --cmd-fetch '...' --cmd-write '...'")
+    write_md(a.out, s, a.cmd_fetch, a.cmd_write, parse_cmd)
+    for st in STAGES:
+        e = s["stages"][st]
+        print(f"{st:26s} {e['traffic_bytes'] / 1e9:10.3f} GB  {e['kernel']}")
+
+
+if __name__ == "__main__":
+    main()
