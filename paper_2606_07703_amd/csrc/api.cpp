@@ -176,6 +176,8 @@ int sp_sparse_gqa_attn(const sp_problem *p, const void *q, const void *k, const 
   const Prob r = resolve(p);
   if (sparse_block_mfma_supported(r))
     return launched(launch_sparse_block_mfma(r, q, k, v, idx, o, stream));
+  if (sparse_query_mfma_supported(r))
+    return launched(launch_sparse_query_mfma(r, q, k, v, idx, o, stream));
   return launched(launch_attn_rowwise(r, q, k, v, idx, o, nullptr, stream));
 }
 

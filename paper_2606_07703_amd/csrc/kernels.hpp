@@ -23,6 +23,9 @@ hipError_t launch_attn_rowwise(const Prob &p, const void *q, const void *k, cons
 
 // bf16 MFMA sparse attention for selection blocks of b >= 16 queries: each
 // gathered K/V row is shared by the b*G query rows of a KV head.
+bool sparse_query_mfma_supported(const Prob &p);
+hipError_t launch_sparse_query_mfma(const Prob &p, const void *q, const void *k, const void *v,
+                                    const int32_t *idx, void *o, hipStream_t st);
 bool sparse_block_mfma_supported(const Prob &p);
 hipError_t launch_sparse_block_mfma(const Prob &p, const void *q, const void *k, const void *v,
                                     const int32_t *idx, void *o, hipStream_t st);

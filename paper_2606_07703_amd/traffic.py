@@ -37,12 +37,12 @@ STAGE_KERNEL_FILE = {
     "block64.sparse_attn": "sparse_block_mfma.hip",
     "perquery.indexer_scores": "indexer_mfma.hip",
     "perquery.topk": "topk.hip",
-    "perquery.sparse_attn": "attn_rowwise.hip",
+    "perquery.sparse_attn": "sparse_query_mfma.hip",
     "dense.attn": "dense_mfma.hip",
     "oracle.normalisers": "dense_mfma.hip",
     "oracle.mass": "mass_mfma.hip",
     "oracle.topk": "topk.hip",
-    "oracle.sparse_attn": "attn_rowwise.hip",
+    "oracle.sparse_attn": "sparse_query_mfma.hip",
 }
 STAGES = list(STAGE_KERNEL_FILE)
 

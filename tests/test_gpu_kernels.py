@@ -43,6 +43,10 @@ SPARSE_CASES = [
     (200, 8, 8, 128, "bf16", 1, 250),
     (520, 32, 8, 128, "bf16", 64, 256),
     (520, 32, 8, 128, "bf16", 128, 96),
+    (300, 32, 2, 64, "bf16", 1, 100),      # G = 16: every MFMA column a head
+    (400, 12, 4, 128, "bf16", 1, 33),      # G = 3, ragged last tile
+    (260, 4, 1, 64, "bf16", 3, 2100),      # support row longer than one LDS chunk
+    (130, 34, 2, 64, "bf16", 1, 40),       # G = 17: row-wise path
 ]
 
 
@@ -63,7 +67,7 @@ def test_sparse_attention(case):
 
 
 @pytest.mark.parametrize("dtype,b,d", [("f32", 16, 128), ("bf16", 64, 128), ("bf16", 16, 64),
-                                       ("bf16", 128, 128)])
+                                       ("bf16", 128, 128), ("bf16", 1, 128), ("bf16", 4, 64)])
 def test_sparse_attention_order_and_sentinels(dtype, b, d):
     S, Hq, Hkv, k = 300, 8, 2, 64
     say(f"sparse shuffled support {dtype} b={b} d={d}")
