@@ -65,7 +65,8 @@ typedef enum sp_status {
   SP_OK = 0,
   SP_ERR_NULL = -1,        /* a required pointer is NULL */
   SP_ERR_SHAPE = -2,       /* inconsistent sizes (e.g. Hq % Hkv != 0, k < 1) */
-  SP_ERR_UNSUPPORTED = -3, /* valid but not built: head_dim, dtype, causal=0 */
+  SP_ERR_UNSUPPORTED = -3, /* valid but not built: head_dim, dtype, causal=0,
+                              k or v of 4 GiB or more */
   SP_ERR_WORKSPACE = -4,   /* workspace smaller than sp_workspace_bytes */
   SP_ERR_ALIGN = -5,       /* a pointer is not 16-byte aligned */
   SP_ERR_NO_DEVICE = -6,   /* no HIP device is usable */
@@ -84,7 +85,7 @@ enum { SP_OP_DENSE = 0, SP_OP_ORACLE = 1, SP_OP_INDEXER = 2, SP_OP_TOPK = 3,
  * attention: |S_t| <= k; Section 6.3: d_idx).
  */
 typedef struct sp_problem {
-  int32_t seq_len;      /* S >= 1 */
+  int32_t seq_len;      /* S >= 1; k and v ([S,Hkv,d]) each below 4 GiB */
   int32_t num_q_heads;  /* Hq >= 1, a multiple of num_kv_heads */
   int32_t num_kv_heads; /* Hkv >= 1 */
   int32_t head_dim;     /* d: 64 or 128 */

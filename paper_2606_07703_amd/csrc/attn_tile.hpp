@@ -33,6 +33,8 @@ namespace sp {
 constexpr int kAttnKT = 64;      // key positions per tile
 constexpr int kAttnQPW = 32;     // query rows per wave
 constexpr float kLazy = 8.f;     // max may lag by up to 8 (factor 256)
+// Word 3 of a raw buffer resource on gfx950: 32-bit data format, no swizzle.
+constexpr int kBufferDword3 = 0x00020000;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 
@@ -73,21 +75,30 @@ struct KVStage {
   __device__ __forceinline__ void load(const uint16_t *__restrict__ k,
                                        const uint16_t *__restrict__ v, int S, int Hkv, int j,
                                        int tid, POS pos) {
-    size_t off[PER];
+    // Rows are fetched through buffer resources (base and size in SGPRs,
+    // 32-bit byte offsets per lane): one multiply-add per piece instead of
+    // 64-bit address arithmetic. The API keeps k and v below 4 GiB.
+    const uint32_t nbytes = (uint32_t)S * Hkv * D * 2;
+    const auto krs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(k), (short)0,
+                                                       nbytes, kBufferDword3);
+    const auto vrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(v), (short)0,
+                                                       nbytes, kBufferDword3);
+    uint32_t off[PER];
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int c = tid + i * NT;
       const int key = c / (D / 8), col = c % (D / 8);
       int s = c < PIECES ? pos(key) : 0;
       s = (s >= 0 && s < S) ? s : 0;
-      off[i] = ((size_t)s * Hkv + j) * D + col * 8;
+      off[i] = ((uint32_t)s * Hkv + j) * (D * 2) + col * 16;
     }
     if (tid < kAttnKT) spos = pos(tid);
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       if (tid + i * NT < PIECES) {
-        kreg[i] = ldg16(k + off[i]);
-        if constexpr (WANT_V) vreg[i] = ldg16(v + off[i]);
+        kreg[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(krs, off[i], 0, 0));
+        if constexpr (WANT_V)
+          vreg[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(vrs, off[i], 0, 0));
       }
     }
   }
@@ -126,7 +137,11 @@ struct AttnState {
   f32x4 oacc[AttnLayout<D>::DT][2];
   float m[2];   // running max (base-2 scaled logits), possibly lagging by < kLazy
   float l[2];   // this lane's share of the row sum (reduce over g at the end)
+  // Row sums taken on the matrix cores (attn_tile MFMA_SUM): a ones A
+  // operand times P^T puts each row's sum in every C row.
+  f32x4 lsum[2];
   __device__ __forceinline__ void init() {
+    lsum[0] = lsum[1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int dt = 0; dt < AttnLayout<D>::DT; ++dt)
 #pragma unroll
@@ -137,8 +152,11 @@ struct AttnState {
 };
 
 // One tile: scores, mask, online softmax, and (WANT_O) the P V product.
-// wave_tmin is the smallest query of the wave's valid rows.
-template <int D, bool WANT_O>
+// wave_tmin is the smallest query of the wave's valid rows. MFMA_SUM (with
+// WANT_O) takes the row sums from the matrix cores, over the same bf16
+// probabilities that weight V; otherwise they are fp32 vector sums (kept
+// where the log-sum-exp is an output).
+template <int D, bool WANT_O, bool MFMA_SUM = false>
 __device__ __forceinline__ void attn_tile(const char *buf, const bf16x8 (&bq)[2][AttnLayout<D>::KS],
                                           const int (&qt)[2], float scale_log2, int wave_tmin,
                                           AttnState<D> &st, int g, int c16) {
@@ -199,9 +217,9 @@ __device__ __forceinline__ void attn_tile(const char *buf, const bf16x8 (&bq)[2]
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         pv[kt][rr] = fast_exp2(fmaf(sacc[kt][qc][rr], scale_log2, -mref));
-        psum += pv[kt][rr];
+        if constexpr (!MFMA_SUM) psum += pv[kt][rr];
       }
-    st.l[qc] = st.l[qc] * corr[qc] + psum;
+    if constexpr (!MFMA_SUM) st.l[qc] = st.l[qc] * corr[qc] + psum;
     if constexpr (WANT_O) {
 #pragma unroll
       for (int f = 0; f < 2; ++f) {
@@ -223,6 +241,22 @@ __device__ __forceinline__ void attn_tile(const char *buf, const bf16x8 (&bq)[2]
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr) st.oacc[dt][qc][rr] *= corr[qc];
+      if constexpr (MFMA_SUM) {
+#pragma unroll
+        for (int qc = 0; qc < 2; ++qc)
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) st.lsum[qc][rr] *= corr[qc];
+      }
+    }
+    if constexpr (MFMA_SUM) {
+      // one MFMA per 32 keys and 16 rows instead of 32 vector adds per tile
+      bf16x8 ones;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
+#pragma unroll
+      for (int qc = 0; qc < 2; ++qc)
+#pragma unroll
+        for (int f = 0; f < 2; ++f) st.lsum[qc] = mfma16(ones, pfrag[qc][f], st.lsum[qc]);
     }
     // O^T += V^T P^T. Lane (g, c16) of the V^T fragment needs d = 16dt + c16
     // and keys 32f + 4g + {0..3} (then +16): each transpose read has the 16
@@ -281,6 +315,7 @@ __device__ __forceinline__ void attn_finish(AttnState<D> &st, const int (&qt)[2]
     float l = st.l[qc];
     l += __shfl_xor(l, 16, 64);
     l += __shfl_xor(l, 32, 64);
+    l += st.lsum[qc][0];
     if (!qvalid[qc]) continue;
     if (lse && g == 0)
       lse[(size_t)qt[qc] * Hq + qh[qc]] = l > 0.f ? (st.m[qc] + log2f(l)) * kLn2 : -INFINITY;

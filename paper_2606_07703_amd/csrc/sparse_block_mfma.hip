@@ -78,7 +78,7 @@ __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
   for (int it = 0; it < ntiles; ++it) {
     const bool more = it + 1 < ntiles;
     if (more) stage.load(k, v, S, Hkv, j, tid, pos_of((it + 1) * kAttnKT));
-    if (live) attn_tile<D, true>(lds[it & 1], bq, qt, scale_log2, wave_tmin, st, g, c16);
+    if (live) attn_tile<D, true, true>(lds[it & 1], bq, qt, scale_log2, wave_tmin, st, g, c16);
     if (more) stage.store(lds[(it + 1) & 1], tid);
     __syncthreads();
   }

@@ -97,6 +97,8 @@ def test_null_pointers():
     (dict(head_dim=96), UNSUP),
     (dict(causal=0), UNSUP),
     (dict(num_q_heads=512, num_kv_heads=2), UNSUP),
+    # k and v of 4 GiB each (rows are addressed with 32-bit byte offsets)
+    (dict(seq_len=1 << 21, num_q_heads=8, num_kv_heads=8, head_dim=128, dtype="bf16"), UNSUP),
 ])
 def test_shape_errors_attention(kw, expect):
     assert dense(prob(**kw)) == expect
