@@ -12,7 +12,10 @@ in the paper's order:
   block aggregation -> top-k -> restricted attention;
 * indexer mode (Algorithm 2, steps 4-5): indexer scores -> block aggregation
   -> top-k -> restricted attention;
-* dense attention (Section 3).
+* dense attention (Section 3);
+* the KL distillation objective and its gradient (Section 6.2);
+* the head-collapsed indexer front end: projection, key LayerNorm, RoPE
+  (Section 6.3, Algorithm 2 steps 2-3).
 
 Parity pins for every function live in ``tests/test_oracle_pins.py``.
 """
@@ -58,8 +61,10 @@ def _load():
         lib.orc_block_aggregate.argtypes = [I, I, I, P, P, P]
         lib.orc_topk.argtypes = [I, P, P, ctypes.c_int64, I, I, P]
         lib.orc_sparse.argtypes = [I, I, I, I, D, P, P, P, I, I, P, I, P, P]
+        lib.orc_kl.argtypes = [I, I, P, P, P, P, P]
+        lib.orc_project.argtypes = [I, I, I, P, P, P, P, P, D, D, I, I, P, P, P]
         for f in ("orc_dense", "orc_mass", "orc_index_scores", "orc_block_aggregate",
-                  "orc_topk", "orc_sparse"):
+                  "orc_topk", "orc_sparse", "orc_kl", "orc_project"):
             getattr(lib, f).restype = None
         _lib = lib
     return _lib
@@ -168,6 +173,40 @@ def sparse(q, k, v, idx, block_q: int, rows=None, scale: Optional[float] = None)
     _load().orc_sparse(S, Hq, Hkv, d, scale, _ptr(q), _ptr(k), _ptr(v), block_q,
                        idx.shape[1], _ptr(idx), len(rows), _ptr(rows), _ptr(o))
     return o
+
+
+def kl(P, z, rows):
+    """KL(P_i || softmax(z_i)) over s <= rows[i] (Section 6.2).
+
+    P, z are [n,S]. Returns (kl [n], grad [n,S]) where grad is the gradient of
+    the mean over rows, L = (1/n) sum_i kl[i], with respect to z.
+    """
+    P, z = _f64(P), _f64(z)
+    rows = _i32(rows)
+    n, S = P.shape
+    out = np.zeros(n)
+    grad = np.zeros((n, S))
+    _load().orc_kl(S, n, _ptr(rows), _ptr(P), _ptr(z), _ptr(out), _ptr(grad))
+    return out, grad
+
+
+def project(x, wq, wk, gamma, beta, rows=None, pos0: int = 0, theta: float = 10000.0,
+            eps: float = 1e-6):
+    """Indexer front end (Section 6.3; Algorithm 2 steps 2-3).
+
+    x [S,dm], wq/wk [d_idx,dm], gamma/beta [d_idx]. Returns (q_idx, k_idx),
+    each [n,d_idx]: RoPE(W_Q x_t) and RoPE(LN(W_K x_t)) at positions pos0 + t.
+    """
+    x, wq, wk = _f64(x), _f64(wq), _f64(wk)
+    gamma, beta = _f64(gamma), _f64(beta)
+    S, dm = x.shape
+    di = wq.shape[0]
+    rows = _rows(S, rows)
+    qo = np.zeros((len(rows), di))
+    ko = np.zeros((len(rows), di))
+    _load().orc_project(S, dm, di, _ptr(x), _ptr(wq), _ptr(wk), _ptr(gamma), _ptr(beta),
+                        eps, theta, pos0, len(rows), _ptr(rows), _ptr(qo), _ptr(ko))
+    return qo, ko
 
 
 # ----------------------------------------------------------------- pipelines

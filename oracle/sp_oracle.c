@@ -260,3 +260,101 @@ void orc_sparse(int S, int Hq, int Hkv, int d, double scale, const double *q,
     free(U);
   }
 }
+
+/*
+ * KL distillation objective (Section 6.2):
+ *   L = (1/n) * sum_i KL(P_i || softmax(z_i)),
+ *   KL(P || Q) = sum_s P(s) * (log P(s) - log Q(s)),   0 * log 0 = 0,
+ * with the softmax over the valid causal keys s <= t_i only:
+ *   log Q(s) = z(s) - log sum_{s' <= t_i} exp(z(s')).
+ * P is taken as given (a teacher row of the head-averaged mass sums to 1).
+ * Gradient of L with respect to z_i(s), s <= t_i:
+ *   dL/dz_i(s) = (Q(s) * sum_{s'} P(s') - P(s)) / n,   and 0 for s > t_i.
+ * P, z and grad are [n, S]; row i belongs to query t_i = rows[i]. A row with
+ * t_i outside [0, S) has KL 0 and gradient 0. kl or grad may be NULL.
+ */
+void orc_kl(int S, int n, const int32_t *rows, const double *P, const double *z,
+            double *kl, double *grad) {
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int i = 0; i < n; ++i) {
+    int t = rows[i];
+    const double *Pi = P + (size_t)i * S;
+    const double *zi = z + (size_t)i * S;
+    double *gi = grad ? grad + (size_t)i * S : NULL;
+    if (gi)
+      for (int s = 0; s < S; ++s) gi[s] = 0.0;
+    if (t < 0 || t >= S) {
+      if (kl) kl[i] = 0.0;
+      continue;
+    }
+    double lz = log_normaliser(zi, t + 1);
+    double sumP = 0.0, acc = 0.0;
+    for (int s = 0; s <= t; ++s) {
+      sumP += Pi[s];
+      if (Pi[s] > 0.0) acc += Pi[s] * (log(Pi[s]) - (zi[s] - lz));
+    }
+    if (kl) kl[i] = acc;
+    if (gi)
+      for (int s = 0; s <= t; ++s) gi[s] = (exp(zi[s] - lz) * sumP - Pi[s]) / n;
+  }
+}
+
+/*
+ * Head-collapsed indexer front end (Section 6.3, first two equations;
+ * Algorithm 2 steps 2-3), for token rows t = rows[i] at positions pos0 + t:
+ *   q = W_Q x_t,   k = LN(W_K x_t),
+ *   LN(a) = (a - mean(a)) / sqrt(var(a) + eps) * gamma + beta   (over d_idx),
+ *   q_idx = RoPE(q, pos0 + t),   k_idx = RoPE(k, pos0 + t),
+ * where RoPE(a, p) rotates each pair (a[c], a[c + d_idx/2]), c < d_idx/2, by
+ * the angle p * theta^(-2c/d_idx):
+ *   out[c]           = a[c] cos - a[c + d_idx/2] sin
+ *   out[c + d_idx/2] = a[c + d_idx/2] cos + a[c] sin.
+ * The 1/sqrt(d_idx) query scale is left to the scorer. x is [S, dm]; wq and
+ * wk are [d_idx, dm]; gamma, beta [d_idx]; q_idx, k_idx [nrows, d_idx].
+ */
+static void rope_row(int di, double p, double theta, const double *a, double *out) {
+  int h = di / 2;
+  for (int c = 0; c < h; ++c) {
+    double ang = p * pow(theta, -2.0 * c / di);
+    double cs = cos(ang), sn = sin(ang);
+    out[c] = a[c] * cs - a[c + h] * sn;
+    out[c + h] = a[c + h] * cs + a[c] * sn;
+  }
+}
+
+void orc_project(int S, int dm, int di, const double *x, const double *wq, const double *wk,
+                 const double *gamma, const double *beta, double eps, double theta, int pos0,
+                 int nrows, const int32_t *rows, double *q_idx, double *k_idx) {
+#pragma omp parallel
+  {
+    double *a = (double *)malloc(sizeof(double) * (size_t)di);
+    double *b = (double *)malloc(sizeof(double) * (size_t)di);
+#pragma omp for schedule(static)
+    for (int i = 0; i < nrows; ++i) {
+      int t = rows[i];
+      const double *xt = x + (size_t)t * dm;
+      double p = (double)pos0 + t;
+      for (int c = 0; c < di; ++c) {
+        double acc = 0.0;
+        for (int e = 0; e < dm; ++e) acc += wq[(size_t)c * dm + e] * xt[e];
+        a[c] = acc;
+      }
+      rope_row(di, p, theta, a, q_idx + (size_t)i * di);
+      for (int c = 0; c < di; ++c) {
+        double acc = 0.0;
+        for (int e = 0; e < dm; ++e) acc += wk[(size_t)c * dm + e] * xt[e];
+        a[c] = acc;
+      }
+      double mean = 0.0, var = 0.0;
+      for (int c = 0; c < di; ++c) mean += a[c];
+      mean /= di;
+      for (int c = 0; c < di; ++c) var += (a[c] - mean) * (a[c] - mean);
+      var /= di;
+      double inv = 1.0 / sqrt(var + eps);
+      for (int c = 0; c < di; ++c) b[c] = (a[c] - mean) * inv * gamma[c] + beta[c];
+      rope_row(di, p, theta, b, k_idx + (size_t)i * di);
+    }
+    free(a);
+    free(b);
+  }
+}

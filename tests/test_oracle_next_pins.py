@@ -1,0 +1,170 @@
+"""Pins for the oracle's KL objective and indexer front end (no GPU).
+
+Each check ties the fp64 oracle to something other than itself: scipy's
+relative entropy, closed forms, finite differences, torch's CPU LayerNorm,
+numpy's matmul, and the algebraic properties of rotary position encoding.
+"""
+import numpy as np
+import pytest
+import scipy.special as ssp
+import scipy.stats as sst
+import torch
+
+import oracle
+
+
+def _rows_pz(n, S, seed, zero_frac=0.0):
+    rng = np.random.default_rng(seed)
+    rows = rng.integers(0, S, size=n).astype(np.int32)
+    rows[0] = S - 1
+    P = np.zeros((n, S))
+    z = rng.normal(size=(n, S)) * 2.0
+    for i, t in enumerate(rows):
+        p = rng.dirichlet(np.ones(t + 1))
+        if zero_frac > 0:
+            p[rng.random(t + 1) < zero_frac] = 0.0
+            if p.sum() == 0:
+                p[0] = 1.0
+            p /= p.sum()
+        P[i, : t + 1] = p
+        P[i, t + 1:] = rng.random(S - t - 1)        # beyond t: must be ignored
+    return rows, P, z
+
+
+# ----------------------------------------------------------------------- KL
+@pytest.mark.parametrize("zero_frac", [0.0, 0.3])
+def test_kl_matches_scipy_relative_entropy(zero_frac):
+    rows, P, z = _rows_pz(9, 40, seed=1, zero_frac=zero_frac)
+    kl, _ = oracle.kl(P, z, rows)
+    for i, t in enumerate(rows):
+        q = ssp.softmax(z[i, : t + 1])
+        assert kl[i] == pytest.approx(sst.entropy(P[i, : t + 1], q), rel=1e-12, abs=1e-14)
+
+
+def test_kl_zero_when_student_matches_teacher():
+    rows, P, _ = _rows_pz(6, 30, seed=2)
+    z = np.where(P > 0, np.log(np.maximum(P, 1e-300)), -5.0) + 3.7   # shift-invariant
+    kl, grad = oracle.kl(P, z, rows)
+    assert np.max(np.abs(kl)) < 1e-12
+    assert np.max(np.abs(grad)) < 1e-12
+
+
+def test_kl_one_hot_teacher_closed_form():
+    S = 25
+    rng = np.random.default_rng(3)
+    rows = np.array([0, 7, 24], dtype=np.int32)
+    z = rng.normal(size=(3, S))
+    P = np.zeros((3, S))
+    star = [0, 3, 20]
+    for i, s in enumerate(star):
+        P[i, s] = 1.0
+    kl, _ = oracle.kl(P, z, rows)
+    for i, t in enumerate(rows):
+        assert kl[i] == pytest.approx(ssp.logsumexp(z[i, : t + 1]) - z[i, star[i]], rel=1e-12)
+
+
+def test_kl_gradient_matches_finite_differences():
+    rows, P, z = _rows_pz(3, 7, seed=4)
+    _, grad = oracle.kl(P, z, rows)
+    h = 1e-6
+    for i in range(3):
+        for s in range(7):
+            zp, zm = z.copy(), z.copy()
+            zp[i, s] += h
+            zm[i, s] -= h
+            fd = (oracle.kl(P, zp, rows)[0].mean() - oracle.kl(P, zm, rows)[0].mean()) / (2 * h)
+            assert grad[i, s] == pytest.approx(fd, abs=1e-8)
+
+
+def test_kl_ignores_entries_after_t_and_bad_rows():
+    rows, P, z = _rows_pz(5, 20, seed=5)
+    kl, grad = oracle.kl(P, z, rows)
+    P2, z2 = P.copy(), z.copy()
+    for i, t in enumerate(rows):
+        P2[i, t + 1:] = 7.0
+        z2[i, t + 1:] = -9.0
+    kl2, grad2 = oracle.kl(P2, z2, rows)
+    assert np.array_equal(kl, kl2) and np.array_equal(grad, grad2)
+    for i, t in enumerate(rows):
+        assert np.all(grad[i, t + 1:] == 0.0)
+        # the gradient of each row sums to zero (softmax sums to one)
+        assert abs(grad[i].sum()) < 1e-14
+    bad = rows.copy()
+    bad[1], bad[2] = -1, 20
+    kl3, grad3 = oracle.kl(P, z, bad)
+    assert kl3[1] == 0.0 and kl3[2] == 0.0
+    assert np.all(grad3[1] == 0.0) and np.all(grad3[2] == 0.0)
+
+
+def test_kl_nonnegative_for_distributions():
+    rows, P, z = _rows_pz(30, 50, seed=6, zero_frac=0.2)
+    kl, _ = oracle.kl(P, z, rows)
+    assert np.all(kl >= -1e-14)
+
+
+# ---------------------------------------------------------------- front end
+def _proj_inputs(S, dm, di, seed, affine=True):
+    rng = np.random.default_rng(seed)
+    x = rng.normal(size=(S, dm))
+    wq = rng.normal(size=(di, dm)) / np.sqrt(dm)
+    wk = rng.normal(size=(di, dm)) / np.sqrt(dm)
+    gamma = 1.0 + 0.1 * rng.normal(size=di) if affine else np.ones(di)
+    beta = 0.1 * rng.normal(size=di) if affine else np.zeros(di)
+    return x, wq, wk, gamma, beta
+
+
+def test_project_position_zero_is_gemm_and_layernorm():
+    x, wq, wk, gamma, beta = _proj_inputs(9, 48, 16, seed=7)
+    q0, k0 = oracle.project(x, wq, wk, gamma, beta, rows=[0], pos0=0)
+    assert np.allclose(q0[0], wq @ x[0], rtol=1e-12, atol=1e-12)
+    ref = torch.nn.functional.layer_norm(torch.from_numpy(wk @ x[0]), (16,),
+                                         torch.from_numpy(gamma), torch.from_numpy(beta),
+                                         eps=1e-6).numpy()
+    assert np.allclose(k0[0], ref, rtol=1e-10, atol=1e-12)
+
+
+def test_project_layernorm_standardises_keys():
+    x, wq, wk, gamma, beta = _proj_inputs(5, 32, 16, seed=8, affine=False)
+    # position 0 so RoPE is the identity
+    _, k0 = oracle.project(x, wq, wk, gamma, beta, rows=[0], pos0=0)
+    assert abs(k0[0].mean()) < 1e-12
+    assert k0[0].var() == pytest.approx(1.0, rel=1e-4)   # var / (var + eps)
+
+
+def test_rope_is_a_rotation_of_each_pair():
+    # d_idx = 2: a single pair rotated by the angle pos * theta^0 = pos
+    x, wq, wk, gamma, beta = _proj_inputs(6, 4, 2, seed=9)
+    q, _ = oracle.project(x, wq, wk, gamma, beta, pos0=0)
+    for t in range(6):
+        a = wq @ x[t]
+        c, s = np.cos(t), np.sin(t)
+        assert np.allclose(q[t], [a[0] * c - a[1] * s, a[1] * c + a[0] * s], atol=1e-12)
+
+
+def test_rope_preserves_norms_and_depends_on_relative_position():
+    S, dm, di = 12, 40, 32
+    x, wq, wk, gamma, beta = _proj_inputs(S, dm, di, seed=10)
+    q, k = oracle.project(x, wq, wk, gamma, beta, pos0=0)
+    q2, k2 = oracle.project(x, wq, wk, gamma, beta, pos0=1000)
+    raw_q = x @ wq.T
+    assert np.allclose(np.linalg.norm(q, axis=1), np.linalg.norm(raw_q, axis=1), rtol=1e-12)
+    # scores depend on the position difference only: shifting every position
+    # by 1000 leaves the score matrix unchanged, while the vectors move
+    assert np.allclose(q @ k.T, q2 @ k2.T, rtol=1e-9, atol=1e-9)
+    assert not np.allclose(q[1:], q2[1:])
+
+
+def test_rope_frequency_schedule():
+    # the pair c rotates by pos * theta^(-2c/d): with x such that W_Q x_t is the
+    # unit vector e_c at every t, q_idx[t] traces that angle
+    S, di = 5, 8
+    for c in range(di // 2):
+        x = np.ones((S, 1))
+        wq = np.zeros((di, 1))
+        wq[c, 0] = 1.0
+        wk = np.ones((di, 1))
+        q, _ = oracle.project(x, wq, wk, np.ones(di), np.zeros(di), pos0=3, theta=500.0)
+        for t in range(S):
+            ang = (3 + t) * 500.0 ** (-2.0 * c / di)
+            assert q[t, c] == pytest.approx(np.cos(ang), abs=1e-12)
+            assert q[t, c + di // 2] == pytest.approx(np.sin(ang), abs=1e-12)
