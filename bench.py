@@ -8,6 +8,8 @@ stage of the path once, on one HIP stream, with inputs resident in HBM:
   2. indexer mode, per-query selection:       scores -> top-k -> sparse attn
   3. dense causal GQA attention (the library's own dense kernel)
   4. oracle mode, per-query: dense normalisers -> mass -> top-k -> sparse attn
+  5. the indexer's KL distillation objective and gradient, with the oracle
+     mass rows of (4) as teacher and the per-query scores of (2) as student
 
 `value` is the ms per layer of (1), the selection-block-shared sparse prefill;
 the per-query and oracle-mode times, the dense time and the speedups are
@@ -99,6 +101,12 @@ def main():
     buf_q = PL.Buffers.for_problem(pq)
     buf_o = PL.Buffers.for_problem(pq, oracle=True)
     o_dense = torch.empty(S, Hq, d, dtype=dev.q.dtype, device="cuda")
+    # KL distillation objective: teacher = oracle mass rows, student = per-query
+    # indexer scores, every query row supervised
+    kl_rows = torch.arange(S, dtype=torch.int32, device="cuda")
+    kl_val = torch.empty(S, device="cuda")
+    kl_loss = torch.empty(1, device="cuda")
+    kl_grad = torch.empty(S, S, device="cuda")
     stream = torch.cuda.current_stream()
 
     stages = [
@@ -113,6 +121,8 @@ def main():
         ("oracle.mass", lambda: B.sp_oracle_support(pq, dev.q, dev.k, buf_o.lse, buf_o.scores)),
         ("oracle.topk", lambda: B.sp_topk_select(pq, buf_o.scores, buf_o.idx)),
         ("oracle.sparse_attn", lambda: B.sp_sparse_gqa_attn(pq, dev.q, dev.k, dev.v, buf_o.idx, buf_o.o)),
+        ("kl.loss", lambda: B.sp_kl_loss(pq, kl_rows, buf_o.scores, buf_q.scores, kl_val, kl_loss,
+                                         kl_grad)),
     ]
 
     def step(events=None):
@@ -180,6 +190,8 @@ def main():
         "oracle.mass": ("mfma", 2.0 * d * Hq * C, 4.0 * C),
         "oracle.topk": ("hbm", None, 4.0 * C + 4.0 * S * k),
         "oracle.sparse_attn": ("hbm", sparse_flops(idx_o, 1), sparse_bytes(idx_o, 1)),
+        # read P and z on s <= t, write the full gradient rows
+        "kl.loss": ("hbm", None, 2 * 4.0 * C + 4.0 * S * S + 8.0 * S),
     }
     kernels = {}
     for name, (bound, flops, nbytes) in work.items():

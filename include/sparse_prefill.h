@@ -77,7 +77,7 @@ typedef enum sp_status {
 enum { SP_DTYPE_F32 = 0, SP_DTYPE_BF16 = 1 };
 enum { SP_AGG_MAX = 0, SP_AGG_SUM = 1 };
 enum { SP_OP_DENSE = 0, SP_OP_ORACLE = 1, SP_OP_INDEXER = 2, SP_OP_TOPK = 3,
-       SP_OP_SPARSE = 4 };
+       SP_OP_SPARSE = 4, SP_OP_KL = 5 };
 
 /*
  * One GQA layer's sparse-prefill problem (Section 3: S, Hq, Hkv, d_h, the
@@ -163,6 +163,26 @@ int sp_topk_select(const sp_problem *p, const float *scores, int32_t *idx, void 
  */
 int sp_sparse_gqa_attn(const sp_problem *p, const void *q, const void *k, const void *v,
                        const int32_t *idx, void *o, hipStream_t stream);
+
+/*
+ * KL distillation objective of the indexer and its gradient (Section 6.2,
+ * the loss equation): for supervised query rows t_i = rows[i], i < n_rows,
+ *   kl[i]  = KL(P_i || softmax(z_i)) = sum_{s<=t_i} P_i(s) (log P_i(s) - z_i(s)) + LSE_i * sum_{s<=t_i} P_i(s),
+ *   LSE_i  = log sum_{s<=t_i} exp z_i(s)   (the softmax runs over valid causal keys only),
+ *   *loss  = (1/n_rows) sum_i kl[i],
+ *   grad_z[i,s] = d loss / d z_i(s) = (softmax(z_i)(s) * sum P_i - P_i(s)) / n_rows for s <= t_i,
+ *                 0 for t_i < s < S,
+ * with 0 * log 0 = 0 and P taken as given (a head-averaged mass row, the
+ * teacher of Section 4.1, sums to 1).
+ * P, z, grad_z: device fp32 [n_rows, S], S = p->seq_len, row-major; entries
+ * after t_i are never read. rows: device int32 [n_rows]; a row whose t_i is
+ * outside [0, S) gets kl 0 and a zero gradient row. kl [n_rows] and loss [1]:
+ * device fp32. kl, loss and grad_z may each be NULL, except that loss needs kl.
+ * All buffers are caller-owned; the call is stream-ordered and allocates
+ * nothing. Fields used: seq_len. n_rows = 0 is a no-op.
+ */
+int sp_kl_loss(const sp_problem *p, const int32_t *rows, int32_t n_rows, const float *P,
+               const float *z, float *kl, float *loss, float *grad_z, hipStream_t stream);
 
 /* Device workspace (bytes) an operation needs for problem p; 0 = none. */
 int sp_workspace_bytes(const sp_problem *p, int op, size_t *bytes);

@@ -19,7 +19,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsparse_
 
 SP_DTYPE = {"f32": 0, "bf16": 1}
 SP_AGG = {"max": 0, "sum": 1}
-SP_OP = {"dense": 0, "oracle": 1, "indexer": 2, "topk": 3, "sparse": 4}
+SP_OP = {"dense": 0, "oracle": 1, "indexer": 2, "topk": 3, "sparse": 4, "kl": 5}
 TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
 STATUS = {0: "SP_OK", -1: "SP_ERR_NULL", -2: "SP_ERR_SHAPE", -3: "SP_ERR_UNSUPPORTED",
           -4: "SP_ERR_WORKSPACE", -5: "SP_ERR_ALIGN", -6: "SP_ERR_NO_DEVICE",
@@ -90,12 +90,13 @@ def load() -> ctypes.CDLL:
         lib.sp_indexer_scores.argtypes = [PP, P, P, P, P]
         lib.sp_topk_select.argtypes = [PP, P, P, P, ctypes.c_size_t, P]
         lib.sp_sparse_gqa_attn.argtypes = [PP, P, P, P, P, P, P]
+        lib.sp_kl_loss.argtypes = [PP, P, ctypes.c_int32, P, P, P, P, P, P]
         lib.sp_workspace_bytes.argtypes = [PP, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
         lib.sp_status_string.argtypes = [ctypes.c_int]
         lib.sp_status_string.restype = ctypes.c_char_p
         lib.sp_version.argtypes = []
         for f in ("sp_dense_attn", "sp_oracle_support", "sp_indexer_scores", "sp_topk_select",
-                  "sp_sparse_gqa_attn", "sp_workspace_bytes", "sp_version"):
+                  "sp_sparse_gqa_attn", "sp_kl_loss", "sp_workspace_bytes", "sp_version"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -184,6 +185,17 @@ def sp_sparse_gqa_attn(p: Problem, q, k, v, idx, o, stream=None) -> None:
           _ptr(k, "k", (S, Hkv, d), dt), _ptr(v, "v", (S, Hkv, d), dt),
           _ptr(idx, "idx", (p.num_blocks, p.topk), torch.int32),
           _ptr(o, "o", (S, Hq, d), dt), _stream(stream))
+
+
+def sp_kl_loss(p: Problem, rows, P, z, kl=None, loss=None, grad_z=None, stream=None) -> None:
+    """KL(P_i || softmax(z_i)) over s <= rows[i], the mean loss and its gradient."""
+    S = p.seq_len
+    n = rows.shape[0] if rows is not None else 0
+    c = p.to_c()
+    _call("sp_kl_loss", ctypes.byref(c), _ptr(rows, "rows", (n,), torch.int32), n,
+          _ptr(P, "P", (n, S), torch.float32), _ptr(z, "z", (n, S), torch.float32),
+          _ptr(kl, "kl", (n,), torch.float32), _ptr(loss, "loss", (1,), torch.float32),
+          _ptr(grad_z, "grad_z", (n, S), torch.float32), _stream(stream))
 
 
 def sp_workspace_bytes(p: Problem, op: str) -> int:

@@ -185,9 +185,23 @@ int sp_sparse_gqa_attn(const sp_problem *p, const void *q, const void *k, const 
   return launched(launch_attn_rowwise(r, q, k, v, idx, o, nullptr, stream));
 }
 
+int sp_kl_loss(const sp_problem *p, const int32_t *rows, int32_t n_rows, const float *P,
+               const float *z, float *kl, float *loss, float *grad_z, hipStream_t stream) {
+  if (!p) return SP_ERR_NULL;
+  if (p->seq_len < 1 || n_rows < 0) return SP_ERR_SHAPE;
+  if (n_rows == 0) return SP_OK;
+  if (!rows || !P || !z) return SP_ERR_NULL;
+  if (loss && !kl) return SP_ERR_NULL;   // the mean is taken over the per-row values
+  if (!aligned16(rows) || !aligned16(P) || !aligned16(z) || !aligned16(kl) ||
+      !aligned16(loss) || !aligned16(grad_z))
+    return SP_ERR_ALIGN;
+  SP_TRY(check_device());
+  return launched(launch_kl_loss(p->seq_len, n_rows, rows, P, z, kl, loss, grad_z, stream));
+}
+
 int sp_workspace_bytes(const sp_problem *p, int op, size_t *bytes) {
   if (!p || !bytes) return SP_ERR_NULL;
-  if (op < SP_OP_DENSE || op > SP_OP_SPARSE) return SP_ERR_SHAPE;
+  if (op < SP_OP_DENSE || op > SP_OP_KL) return SP_ERR_SHAPE;
   *bytes = 0;
   return SP_OK;
 }

@@ -43,8 +43,11 @@ STAGE_KERNEL_FILE = {
     "oracle.mass": "mass_mfma.hip",
     "oracle.topk": "topk.hip",
     "oracle.sparse_attn": "sparse_query_mfma.hip",
+    "kl.loss": "kl_loss.hip",
 }
 STAGES = list(STAGE_KERNEL_FILE)
+# kernel launches per stage when not one (per-row KL, then the mean)
+STAGE_DISPATCHES = {"kl.loss": 2}
 
 # kernels of the library (everything else in a trace is torch or the runtime)
 LIB_KERNEL_RE = re.compile(r"sp::|_ZN2sp")
@@ -99,9 +102,10 @@ def summarize(fetch_dir: str, write_dir: str, copy_bytes: int) -> Dict:
         lib = [d for d in ds if LIB_KERNEL_RE.search(d["name"])]
         copies = [d for d in ds if not LIB_KERNEL_RE.search(d["name"])
                   and COPY_KERNEL_RE.search(d["name"])]
-        if len(lib) % len(STAGES):
+        per_step = sum(STAGE_DISPATCHES.get(st, 1) for st in STAGES)
+        if len(lib) % per_step:
             raise ValueError(f"{counter}: {len(lib)} library dispatches is not a whole number "
-                             f"of {len(STAGES)}-stage steps")
+                             f"of {per_step}-dispatch steps")
         if not copies:
             raise ValueError(f"{counter}: no copy dispatch for calibration")
         # the calibration copy is the largest copy dispatch
@@ -109,13 +113,17 @@ def summarize(fetch_dir: str, write_dir: str, copy_bytes: int) -> Dict:
         factor = copy_bytes / (cal_kib * 1024.0)
         out[f"{key}_copy_kib"] = cal_kib
         out[f"{key}_factor"] = factor
-        nsteps = len(lib) // len(STAGES)
-        for i, st in enumerate(STAGES):
-            vals = [lib[s * len(STAGES) + i]["value"] for s in range(nsteps)]
+        nsteps = len(lib) // per_step
+        first = 0
+        for st in STAGES:
+            nd = STAGE_DISPATCHES.get(st, 1)
+            vals = [sum(lib[s * per_step + first + x]["value"] for x in range(nd))
+                    for s in range(nsteps)]
             kib = sum(vals) / len(vals)
-            e = out["stages"].setdefault(st, {"kernel": _short(lib[i]["name"])})
+            e = out["stages"].setdefault(st, {"kernel": _short(lib[first]["name"])})
             e[f"{key}_kib"] = kib
             e[f"{key}_bytes"] = kib * 1024.0 * factor
+            first += nd
     for st, e in out["stages"].items():
         e["traffic_bytes"] = e["fetch_bytes"] + e["write_bytes"]
         files = kernel_sources(STAGE_KERNEL_FILE[st])

@@ -129,3 +129,36 @@ def make_support(seq_len: int, block_q: int, topk: int, seed: int = 0,
             sel = rng.permutation(sel)
         out[r, :m] = sel
     return torch.from_numpy(out)
+
+
+def make_kl_rows(n: int, seq_len: int, seed: int = 0, rows=None, zero_frac: float = 0.0,
+                 tail: float = float("nan"), device="cpu"):
+    """Teacher rows P, student rows z [n, seq_len] fp32 and their query positions.
+
+    Row i belongs to query t_i (``rows``, or uniform in [0, seq_len)). On
+    s <= t_i, P is u^3 for u ~ U(0,1) with a fraction ``zero_frac`` set to
+    exact zeros, normalised to sum 1 (a row drawn all zero puts its mass on
+    position 0); z ~ N(0, 4). Entries after t_i hold ``tail`` (NaN by
+    default) so any read of them shows. Drawn with a seeded torch generator
+    on ``device``, so full-size rows can be made where they are used.
+    """
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    if rows is None:
+        rows = torch.randint(0, seq_len, (n,), generator=g, device=device)
+    rows = torch.as_tensor(rows, device=device).to(torch.int64)
+    s = torch.arange(seq_len, device=device)
+    valid = s[None, :] <= rows[:, None]
+    u = torch.rand(n, seq_len, generator=g, device=device) ** 3
+    if zero_frac > 0:
+        drop = torch.rand(n, seq_len, generator=g, device=device) < zero_frac
+        u = torch.where(drop, torch.zeros((), device=device), u)
+    u = torch.where(valid, u, torch.zeros((), device=device))
+    empty = u.sum(1) == 0
+    u[:, 0] = torch.where(empty, torch.ones((), device=device), u[:, 0])
+    P = u / u.sum(1, keepdim=True)
+    z = torch.randn(n, seq_len, generator=g, device=device) * 2.0
+    fill = torch.full((), tail, device=device)
+    P = torch.where(valid, P, fill).to(torch.float32).contiguous()
+    z = torch.where(valid, z, fill).to(torch.float32).contiguous()
+    return rows.to(torch.int32), P, z

@@ -25,12 +25,21 @@ def _write_run(d, counter, values, copy_kib):
                     "Counter_Name": counter, "Counter_Value": copy_kib})
 
 
+def _per_dispatch(stage_values):
+    """Split each stage's value evenly over its kernel launches."""
+    out = []
+    for st, v in zip(T.STAGES, stage_values):
+        nd = T.STAGE_DISPATCHES.get(st, 1)
+        out += [v / nd] * nd
+    return out
+
+
 def test_summary_scales_by_copy_and_maps_stages(tmp_path):
     n = len(T.STAGES)
     fetch = [100.0 * (i + 1) for i in range(n)]
     write = [10.0 * (i + 1) for i in range(n)]
-    _write_run(tmp_path / "f", "FETCH_SIZE", fetch, copy_kib=512 * 1024)     # reads half
-    _write_run(tmp_path / "w", "WRITE_SIZE", write, copy_kib=1024 * 1024)    # exact
+    _write_run(tmp_path / "f", "FETCH_SIZE", _per_dispatch(fetch), copy_kib=512 * 1024)
+    _write_run(tmp_path / "w", "WRITE_SIZE", _per_dispatch(write), copy_kib=1024 * 1024)
     s = T.summarize(str(tmp_path / "f"), str(tmp_path / "w"), 1 << 30)
     assert s["fetch_factor"] == pytest.approx(2.0)
     assert s["write_factor"] == pytest.approx(1.0)
@@ -60,7 +69,8 @@ def test_changed_source_invalidates(tmp_path):
 
 
 def test_ragged_dispatch_count_rejected(tmp_path):
-    _write_run(tmp_path / "f", "FETCH_SIZE", [1.0] * (len(T.STAGES) + 1), copy_kib=1.0)
-    _write_run(tmp_path / "w", "WRITE_SIZE", [1.0] * len(T.STAGES), copy_kib=1.0)
+    per_step = len(_per_dispatch([1.0] * len(T.STAGES)))
+    _write_run(tmp_path / "f", "FETCH_SIZE", [1.0] * (per_step + 1), copy_kib=1.0)
+    _write_run(tmp_path / "w", "WRITE_SIZE", [1.0] * per_step, copy_kib=1.0)
     with pytest.raises(ValueError):
         T.summarize(str(tmp_path / "f"), str(tmp_path / "w"), 1 << 20)
