@@ -10,6 +10,8 @@ stage of the path once, on one HIP stream, with inputs resident in HBM:
   4. oracle mode, per-query: dense normalisers -> mass -> top-k -> sparse attn
   5. the indexer's KL distillation objective and gradient, with the oracle
      mass rows of (4) as teacher and the per-query scores of (2) as student
+  0. (first) the indexer front end: projection of d_model=4096 hidden states,
+     key LayerNorm and RoPE (random weights)
 
 `value` is the ms per layer of (1), the selection-block-shared sparse prefill;
 the per-query and oracle-mode times, the dense time and the speedups are
@@ -83,7 +85,7 @@ def main():
         sys.exit(2)
     from paper_2606_07703_amd import binding as B
     from paper_2606_07703_amd import pipeline as PL
-    from synth import get_workload, make_inputs
+    from synth import get_workload, make_inputs, make_projection_inputs
 
     w = get_workload(args.workload)
     S, Hq, Hkv, d, di, k = w.seq_len, w.num_q_heads, w.num_kv_heads, w.head_dim, w.index_dim, w.topk
@@ -107,9 +109,15 @@ def main():
     kl_val = torch.empty(S, device="cuda")
     kl_loss = torch.empty(1, device="cuda")
     kl_grad = torch.empty(S, S, device="cuda")
+    # indexer front end on Qwen-like hidden states (d_model 4096, random weights)
+    D_MODEL = 4096
+    px, pwq, pwk, pg, pb_ = (t.cuda() for t in make_projection_inputs(S, D_MODEL, di, seed=w.seed))
+    pqo = torch.empty(S, di, dtype=torch.bfloat16, device="cuda")
+    pko = torch.empty(S, di, dtype=torch.bfloat16, device="cuda")
     stream = torch.cuda.current_stream()
 
     stages = [
+        ("frontend.project", lambda: B.sp_indexer_project(pb, px, pwq, pwk, pg, pb_, pqo, pko)),
         ("block64.indexer_scores", lambda: B.sp_indexer_scores(pb, dev.q_idx, dev.k_idx, buf_b.scores)),
         ("block64.topk", lambda: B.sp_topk_select(pb, buf_b.scores, buf_b.idx)),
         ("block64.sparse_attn", lambda: B.sp_sparse_gqa_attn(pb, dev.q, dev.k, dev.v, buf_b.idx, buf_b.o)),
@@ -179,6 +187,8 @@ def main():
     R_b = pb.num_blocks
     lens_b = np.array([min(r * 64 + 64, S) for r in range(R_b)])
     work = {
+        "frontend.project": ("hbm", 2.0 * S * D_MODEL * 2 * di,
+                             2.0 * (S * D_MODEL + 2 * di * D_MODEL + 2 * S * di) + 8.0 * di),
         "block64.indexer_scores": ("mfma", 2.0 * di * C, None),
         "block64.topk": ("hbm", None, 4.0 * lens_b.sum() + 4.0 * R_b * k),
         "block64.sparse_attn": ("hbm", sparse_flops(idx_b, 64), sparse_bytes(idx_b, 64)),

@@ -77,7 +77,7 @@ typedef enum sp_status {
 enum { SP_DTYPE_F32 = 0, SP_DTYPE_BF16 = 1 };
 enum { SP_AGG_MAX = 0, SP_AGG_SUM = 1 };
 enum { SP_OP_DENSE = 0, SP_OP_ORACLE = 1, SP_OP_INDEXER = 2, SP_OP_TOPK = 3,
-       SP_OP_SPARSE = 4, SP_OP_KL = 5 };
+       SP_OP_SPARSE = 4, SP_OP_KL = 5, SP_OP_PROJECT = 6 };
 
 /*
  * One GQA layer's sparse-prefill problem (Section 3: S, Hq, Hkv, d_h, the
@@ -163,6 +163,30 @@ int sp_topk_select(const sp_problem *p, const float *scores, int32_t *idx, void 
  */
 int sp_sparse_gqa_attn(const sp_problem *p, const void *q, const void *k, const void *v,
                        const int32_t *idx, void *o, hipStream_t stream);
+
+/*
+ * Head-collapsed indexer front end (Section 6.3, the projection equations
+ * and the score equation's RoPE; Algorithm 2 steps 2-3): for token t at
+ * position pos0 + t, with x_t = x[t,:],
+ *   q_idx[t] = RoPE(W_Q x_t, pos0 + t),
+ *   k_idx[t] = RoPE(LN(W_K x_t), pos0 + t),
+ *   LN(a)    = (a - mean(a)) / sqrt(var(a) + ln_eps) * gamma + beta   over the d_idx entries,
+ *   RoPE(a, p): each pair (a[c], a[c + d_idx/2]), c < d_idx/2, is rotated by the
+ *              angle p * rope_theta^(-2c/d_idx):
+ *              (a[c] cos - a[c+d_idx/2] sin, a[c+d_idx/2] cos + a[c] sin).
+ * The 1/sqrt(d_idx) query scale is not applied here (sp_indexer_scores
+ * applies index_scale). The outputs are the q_idx, k_idx inputs of
+ * sp_indexer_scores. x: device bf16 [S, d_model], d_model a multiple of 64;
+ * w_q, w_k: device bf16 [d_idx, d_model] (row c projects onto entry c);
+ * gamma, beta: device fp32 [d_idx]; q_idx, k_idx: device bf16 [S, d_idx]
+ * (outputs). pos0 >= 0 (a chunk of a longer sequence starts at pos0),
+ * rope_theta > 0, ln_eps >= 0. Fields used: seq_len, index_dim, dtype (must be
+ * SP_DTYPE_BF16). Caller-owned memory, stream-ordered, allocates nothing.
+ */
+int sp_indexer_project(const sp_problem *p, int32_t d_model, int32_t pos0, float rope_theta,
+                       float ln_eps, const void *x, const void *w_q, const void *w_k,
+                       const float *gamma, const float *beta, void *q_idx, void *k_idx,
+                       hipStream_t stream);
 
 /*
  * KL distillation objective of the indexer and its gradient (Section 6.2,

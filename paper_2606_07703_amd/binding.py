@@ -19,7 +19,8 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsparse_
 
 SP_DTYPE = {"f32": 0, "bf16": 1}
 SP_AGG = {"max": 0, "sum": 1}
-SP_OP = {"dense": 0, "oracle": 1, "indexer": 2, "topk": 3, "sparse": 4, "kl": 5}
+SP_OP = {"dense": 0, "oracle": 1, "indexer": 2, "topk": 3, "sparse": 4, "kl": 5,
+         "project": 6}
 TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
 STATUS = {0: "SP_OK", -1: "SP_ERR_NULL", -2: "SP_ERR_SHAPE", -3: "SP_ERR_UNSUPPORTED",
           -4: "SP_ERR_WORKSPACE", -5: "SP_ERR_ALIGN", -6: "SP_ERR_NO_DEVICE",
@@ -91,12 +92,15 @@ def load() -> ctypes.CDLL:
         lib.sp_topk_select.argtypes = [PP, P, P, P, ctypes.c_size_t, P]
         lib.sp_sparse_gqa_attn.argtypes = [PP, P, P, P, P, P, P]
         lib.sp_kl_loss.argtypes = [PP, P, ctypes.c_int32, P, P, P, P, P, P]
+        I32, F = ctypes.c_int32, ctypes.c_float
+        lib.sp_indexer_project.argtypes = [PP, I32, I32, F, F, P, P, P, P, P, P, P, P]
         lib.sp_workspace_bytes.argtypes = [PP, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
         lib.sp_status_string.argtypes = [ctypes.c_int]
         lib.sp_status_string.restype = ctypes.c_char_p
         lib.sp_version.argtypes = []
         for f in ("sp_dense_attn", "sp_oracle_support", "sp_indexer_scores", "sp_topk_select",
-                  "sp_sparse_gqa_attn", "sp_kl_loss", "sp_workspace_bytes", "sp_version"):
+                  "sp_sparse_gqa_attn", "sp_kl_loss", "sp_indexer_project",
+                  "sp_workspace_bytes", "sp_version"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -185,6 +189,20 @@ def sp_sparse_gqa_attn(p: Problem, q, k, v, idx, o, stream=None) -> None:
           _ptr(k, "k", (S, Hkv, d), dt), _ptr(v, "v", (S, Hkv, d), dt),
           _ptr(idx, "idx", (p.num_blocks, p.topk), torch.int32),
           _ptr(o, "o", (S, Hq, d), dt), _stream(stream))
+
+
+def sp_indexer_project(p: Problem, x, w_q, w_k, gamma, beta, q_idx, k_idx, pos0: int = 0,
+                       rope_theta: float = 10000.0, ln_eps: float = 1e-6, stream=None) -> None:
+    """q_idx = RoPE(W_Q x), k_idx = RoPE(LN(W_K x)) at positions pos0 + t."""
+    S, di = p.seq_len, p.index_dim
+    dm = x.shape[1] if x is not None and x.dim() == 2 else 0
+    c = p.to_c()
+    bf = torch.bfloat16
+    _call("sp_indexer_project", ctypes.byref(c), dm, pos0, rope_theta, ln_eps,
+          _ptr(x, "x", (S, dm), bf), _ptr(w_q, "w_q", (di, dm), bf),
+          _ptr(w_k, "w_k", (di, dm), bf), _ptr(gamma, "gamma", (di,), torch.float32),
+          _ptr(beta, "beta", (di,), torch.float32), _ptr(q_idx, "q_idx", (S, di), bf),
+          _ptr(k_idx, "k_idx", (S, di), bf), _stream(stream))
 
 
 def sp_kl_loss(p: Problem, rows, P, z, kl=None, loss=None, grad_z=None, stream=None) -> None:

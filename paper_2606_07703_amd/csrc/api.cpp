@@ -185,6 +185,28 @@ int sp_sparse_gqa_attn(const sp_problem *p, const void *q, const void *k, const 
   return launched(launch_attn_rowwise(r, q, k, v, idx, o, nullptr, stream));
 }
 
+int sp_indexer_project(const sp_problem *p, int32_t d_model, int32_t pos0, float rope_theta,
+                       float ln_eps, const void *x, const void *w_q, const void *w_k,
+                       const float *gamma, const float *beta, void *q_idx, void *k_idx,
+                       hipStream_t stream) {
+  if (!p) return SP_ERR_NULL;
+  if (p->seq_len < 1 || d_model < 1 || pos0 < 0) return SP_ERR_SHAPE;
+  if ((int64_t)pos0 + p->seq_len > INT32_MAX) return SP_ERR_SHAPE;
+  if (!(rope_theta > 0.f) || !isfinite(rope_theta) || !(ln_eps >= 0.f) || !isfinite(ln_eps))
+    return SP_ERR_SHAPE;
+  if (p->dtype != SP_DTYPE_BF16) return SP_ERR_UNSUPPORTED;
+  if (p->index_dim != 64 && p->index_dim != 128 && p->index_dim != 256) return SP_ERR_UNSUPPORTED;
+  if (d_model % 64 != 0) return SP_ERR_UNSUPPORTED;
+  if (!x || !w_q || !w_k || !gamma || !beta || !q_idx || !k_idx) return SP_ERR_NULL;
+  if (!aligned16(x) || !aligned16(w_q) || !aligned16(w_k) || !aligned16(gamma) ||
+      !aligned16(beta) || !aligned16(q_idx) || !aligned16(k_idx))
+    return SP_ERR_ALIGN;
+  SP_TRY(check_device());
+  return launched(launch_indexer_project(p->seq_len, p->index_dim, d_model, pos0, rope_theta,
+                                         ln_eps, x, w_q, w_k, gamma, beta, q_idx, k_idx,
+                                         stream));
+}
+
 int sp_kl_loss(const sp_problem *p, const int32_t *rows, int32_t n_rows, const float *P,
                const float *z, float *kl, float *loss, float *grad_z, hipStream_t stream) {
   if (!p) return SP_ERR_NULL;
@@ -201,7 +223,7 @@ int sp_kl_loss(const sp_problem *p, const int32_t *rows, int32_t n_rows, const f
 
 int sp_workspace_bytes(const sp_problem *p, int op, size_t *bytes) {
   if (!p || !bytes) return SP_ERR_NULL;
-  if (op < SP_OP_DENSE || op > SP_OP_KL) return SP_ERR_SHAPE;
+  if (op < SP_OP_DENSE || op > SP_OP_PROJECT) return SP_ERR_SHAPE;
   *bytes = 0;
   return SP_OK;
 }

@@ -53,6 +53,10 @@ hipError_t launch_indexer_mfma(const Prob &p, const void *qi, const void *ki, fl
                                hipStream_t st);
 
 // Row-wise top-k selection.
+hipError_t launch_indexer_project(int S, int di, int dm, int pos0, float theta, float eps,
+                                  const void *x, const void *wq, const void *wk,
+                                  const float *gamma, const float *beta, void *qo, void *ko,
+                                  hipStream_t st);
 hipError_t launch_kl_loss(int S, int n, const int32_t *rows, const float *P, const float *z,
                           float *kl, float *loss, float *grad, hipStream_t st);
 hipError_t launch_topk(const Prob &p, const float *scores, int32_t *idx, hipStream_t st);

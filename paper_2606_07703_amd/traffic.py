@@ -32,6 +32,7 @@ CSRC = os.path.join(PKG, "csrc")
 
 # bench stage -> HIP source of the kernel it launches
 STAGE_KERNEL_FILE = {
+    "frontend.project": "indexer_project.hip",
     "block64.indexer_scores": "indexer_mfma.hip",
     "block64.topk": "topk.hip",
     "block64.sparse_attn": "sparse_block_mfma.hip",

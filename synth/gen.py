@@ -162,3 +162,19 @@ def make_kl_rows(n: int, seq_len: int, seed: int = 0, rows=None, zero_frac: floa
     P = torch.where(valid, P, fill).to(torch.float32).contiguous()
     z = torch.where(valid, z, fill).to(torch.float32).contiguous()
     return rows.to(torch.int32), P, z
+
+
+def make_projection_inputs(seq_len: int, d_model: int, index_dim: int, seed: int = 0):
+    """Hidden states and random indexer-projection weights (the trained ones
+    are not released): x [S, d_model] ~ N(0,1), W_Q and W_K [d_idx, d_model]
+    ~ N(0, 1/d_model), all rounded to bf16; LayerNorm gamma ~ 1 + N(0, 0.01)
+    and beta ~ N(0, 0.01) in fp32. Returns (x, w_q, w_k, gamma, beta)."""
+    rng = _rng(seed)
+    x = rng.standard_normal((seq_len, d_model), dtype=np.float32)
+    sd = np.float32(1.0 / np.sqrt(d_model))
+    wq = rng.standard_normal((index_dim, d_model), dtype=np.float32) * sd
+    wk = rng.standard_normal((index_dim, d_model), dtype=np.float32) * sd
+    gamma = (1.0 + 0.1 * rng.standard_normal(index_dim)).astype(np.float32)
+    beta = (0.1 * rng.standard_normal(index_dim)).astype(np.float32)
+    bf = lambda a: torch.from_numpy(a).to(torch.bfloat16)
+    return bf(x), bf(wq), bf(wk), torch.from_numpy(gamma), torch.from_numpy(beta)

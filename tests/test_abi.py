@@ -163,3 +163,51 @@ def test_binding_rejects_bad_tensors():
     cpu = torch.zeros(16, 4, 64)
     with pytest.raises(ValueError):
         B.sp_dense_attn(p, cpu, cpu, cpu, cpu)
+
+
+def _project_args(**kw):
+    a = dict(d_model=128, pos0=0, theta=10000.0, eps=1e-6)
+    a.update(kw)
+    pc = prob(index_dim=a.pop("index_dim", 64), dtype=a.pop("dtype", "bf16"))
+    P = ctypes.c_void_p
+    buf = [P(16)] * 7
+    nulls = a.pop("nulls", ())
+    for i in nulls:
+        buf[i] = None
+    return (ctypes.byref(pc), a["d_model"], a["pos0"], ctypes.c_float(a["theta"]),
+            ctypes.c_float(a["eps"]), *buf, None)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(d_model=96), UNSUP),
+    (dict(index_dim=96), UNSUP),
+    (dict(dtype="f32"), UNSUP),
+    (dict(pos0=-1), SHAPE),
+    (dict(theta=0.0), SHAPE),
+    (dict(eps=-1.0), SHAPE),
+    (dict(d_model=0), SHAPE),
+    (dict(nulls=(3,)), NULL),
+])
+def test_project_errors(kw, expect):
+    assert lib().sp_indexer_project(*_project_args(**kw)) == expect
+
+
+def test_project_valid_arguments_report_no_device():
+    if not NO_DEVICE:
+        pytest.skip("a device is present")
+    assert lib().sp_indexer_project(*_project_args()) == NODEV
+
+
+def test_kl_errors():
+    P = ctypes.c_void_p
+    pc = prob()
+    f = lib().sp_kl_loss
+    assert f(None, P(16), 1, P(16), P(16), None, None, None, None) == NULL
+    assert f(ctypes.byref(pc), P(16), -1, P(16), P(16), None, None, None, None) == SHAPE
+    assert f(ctypes.byref(pc), P(16), 0, None, None, None, None, None, None) == 0   # no rows
+    assert f(ctypes.byref(pc), P(16), 2, None, P(16), None, None, None, None) == NULL
+    # the mean needs the per-row values
+    assert f(ctypes.byref(pc), P(16), 2, P(16), P(16), None, P(16), None, None) == NULL
+    assert f(ctypes.byref(pc), P(16), 2, P(16), P(18), None, None, None, None) == ALIGN
+    if NO_DEVICE:
+        assert f(ctypes.byref(pc), P(16), 2, P(16), P(16), P(16), P(16), P(16), None) == NODEV

@@ -1,7 +1,8 @@
 """GPU parity of the NEXT-row entry points against the fp64 oracle.
 
-KL distillation loss (sp_kl_loss). Inputs come from the seeded generators
-only; full-size runs are checked on sampled rows.
+KL distillation loss (sp_kl_loss) and the indexer front end
+(sp_indexer_project). Inputs come from the seeded generators only; full-size
+runs are checked on sampled rows.
 """
 import numpy as np
 import pytest
@@ -9,7 +10,7 @@ import torch
 
 import oracle
 from paper_2606_07703_amd import binding as B
-from synth import make_kl_rows
+from synth import make_kl_rows, make_projection_inputs
 
 from helpers import say
 
@@ -105,3 +106,54 @@ def test_kl_loss_full_size_sampled():
               ref_kl, ref_grad)
     # the mean: fp64 sum of the kernel's own per-row values
     assert loss.item() == pytest.approx(kl.double().mean().item(), rel=1e-6)
+
+
+# ---------------------------------------------------------------- front end
+# Outputs are bf16 (round-to-nearest-even: relative error <= 2^-9) of values the
+# kernel forms in fp32 from the same bf16 inputs the oracle reads exactly; the
+# fp32 GEMM, LayerNorm and rotation add errors near 1e-6. Bound: 2^-8 relative
+# plus 1e-4 absolute.
+def _check_proj(got, ref):
+    got = got.float().cpu().double().numpy()
+    err = np.abs(got - ref) - (2.0 ** -8 * np.abs(ref) + 1e-4)
+    assert np.all(err <= 0), f"max excess {err.max():.3e}, max abs err {np.abs(got - ref).max():.3e}"
+
+
+def _project(S, dm, di, pos0, seed, theta=10000.0, eps=1e-6):
+    x, wq, wk, gamma, beta = make_projection_inputs(S, dm, di, seed=seed)
+    p = B.Problem(S, 1, 1, 64, index_dim=di)
+    qo = torch.empty(S, di, dtype=torch.bfloat16, device="cuda")
+    ko = torch.empty(S, di, dtype=torch.bfloat16, device="cuda")
+    B.sp_indexer_project(p, x.cuda(), wq.cuda(), wk.cuda(), gamma.cuda(), beta.cuda(), qo, ko,
+                         pos0=pos0, rope_theta=theta, ln_eps=eps)
+    torch.cuda.synchronize()
+    return (x, wq, wk, gamma, beta), qo, ko
+
+
+@pytest.mark.parametrize("S,dm,di,pos0", [(1, 64, 64, 0), (130, 128, 64, 0),
+                                          (130, 192, 128, 1000), (65, 256, 256, 7),
+                                          (200, 512, 128, 100000)])
+def test_indexer_project(S, dm, di, pos0):
+    say(f"project S={S} d_model={dm} d_idx={di} pos0={pos0}")
+    (x, wq, wk, gamma, beta), qo, ko = _project(S, dm, di, pos0, seed=S + di)
+    rq, rk = oracle.project(x, wq, wk, gamma, beta, pos0=pos0)
+    _check_proj(qo, rq)
+    _check_proj(ko, rk)
+
+
+def test_indexer_project_theta_and_eps():
+    S, dm, di = 70, 128, 128
+    (x, wq, wk, gamma, beta), qo, ko = _project(S, dm, di, 3, seed=1, theta=500000.0, eps=1e-3)
+    rq, rk = oracle.project(x, wq, wk, gamma, beta, pos0=3, theta=500000.0, eps=1e-3)
+    _check_proj(qo, rq)
+    _check_proj(ko, rk)
+
+
+def test_indexer_project_full_size_sampled():
+    S, dm, di = 32768, 4096, 128
+    say(f"project full size S={S} d_model={dm} d_idx={di}")
+    (x, wq, wk, gamma, beta), qo, ko = _project(S, dm, di, 0, seed=4)
+    sample = np.array([0, 1, 63, 64, 4095, 20000, 32704, 32767])
+    rq, rk = oracle.project(x, wq, wk, gamma, beta, rows=sample)
+    _check_proj(qo[sample], rq)
+    _check_proj(ko[sample], rk)
