@@ -5,7 +5,8 @@ bf16, seeded synthetic inputs with 128 planted needles. One step runs every
 stage of the path once, on one HIP stream, with inputs resident in HBM:
 
   1. indexer mode, 64-query selection blocks: scores -> top-k -> sparse attn
-  2. indexer mode, per-query selection:       scores -> top-k -> sparse attn
+  2. indexer mode, per-query selection:       scores -> top-k -> sparse attn,
+     and the fused scores+top-k that never stores the S x S scores
   3. dense causal GQA attention (the library's own dense kernel)
   4. oracle mode, per-query: dense normalisers -> mass -> top-k -> sparse attn
   5. the indexer's KL distillation objective and gradient, with the oracle
@@ -109,6 +110,10 @@ def main():
     kl_val = torch.empty(S, device="cuda")
     kl_loss = torch.empty(1, device="cuda")
     kl_grad = torch.empty(S, S, device="cuda")
+    # fused per-query scoring + top-k (no S x S score buffer)
+    fz_idx = torch.empty(S, k, dtype=torch.int32, device="cuda")
+    fz_ws = torch.empty(B.sp_workspace_bytes(pq, "indexer_topk"), dtype=torch.uint8,
+                        device="cuda")
     # indexer front end on Qwen-like hidden states (d_model 4096, random weights)
     D_MODEL = 4096
     px, pwq, pwk, pg, pb_ = (t.cuda() for t in make_projection_inputs(S, D_MODEL, di, seed=w.seed))
@@ -124,6 +129,8 @@ def main():
         ("perquery.indexer_scores", lambda: B.sp_indexer_scores(pq, dev.q_idx, dev.k_idx, buf_q.scores)),
         ("perquery.topk", lambda: B.sp_topk_select(pq, buf_q.scores, buf_q.idx)),
         ("perquery.sparse_attn", lambda: B.sp_sparse_gqa_attn(pq, dev.q, dev.k, dev.v, buf_q.idx, buf_q.o)),
+        ("perquery.fused_scores_topk", lambda: B.sp_indexer_topk(pq, dev.q_idx, dev.k_idx, fz_idx,
+                                                                 fz_ws)),
         ("dense.attn", lambda: B.sp_dense_attn(pq, dev.q, dev.k, dev.v, o_dense, None)),
         ("oracle.normalisers", lambda: B.sp_dense_attn(pq, dev.q, dev.k, dev.v, None, buf_o.lse)),
         ("oracle.mass", lambda: B.sp_oracle_support(pq, dev.q, dev.k, buf_o.lse, buf_o.scores)),
@@ -195,6 +202,9 @@ def main():
         "perquery.indexer_scores": ("hbm", 2.0 * di * C, 4.0 * C + 2.0 * S * di * elt),
         "perquery.topk": ("hbm", None, 4.0 * C + 4.0 * S * k),
         "perquery.sparse_attn": ("hbm", sparse_flops(idx_q, 1), sparse_bytes(idx_q, 1)),
+        # algorithmic work of one scoring of every causal pair (the passes
+        # recompute it; that is overhead, not work)
+        "perquery.fused_scores_topk": ("mfma", 2.0 * di * C, 2.0 * S * di * elt + 4.0 * S * k),
         "dense.attn": ("mfma", 4.0 * d * Hq * C, None),
         "oracle.normalisers": ("mfma", 2.0 * d * Hq * C, None),
         "oracle.mass": ("mfma", 2.0 * d * Hq * C, 4.0 * C),
@@ -220,6 +230,7 @@ def main():
 
     block_ms = sum(med[n] for n in ("block64.indexer_scores", "block64.topk", "block64.sparse_attn"))
     pq_ms = sum(med[n] for n in ("perquery.indexer_scores", "perquery.topk", "perquery.sparse_attn"))
+    pqf_ms = med["perquery.fused_scores_topk"] + med["perquery.sparse_attn"]
     or_ms = sum(med[n] for n in ("oracle.normalisers", "oracle.mass", "oracle.topk",
                                  "oracle.sparse_attn"))
     dense_ms = med["dense.attn"]
@@ -265,6 +276,7 @@ def main():
         "dense_ms": round(dense_ms, 4),
         "per_query_ms_per_layer": round(pq_ms, 4),
         "per_query_speedup_vs_dense": round(dense_ms / pq_ms, 3),
+        "per_query_fused_ms_per_layer": round(pqf_ms, 4),
         "oracle_mode_ms_per_layer": round(or_ms, 4),
         "roofline": roof,
         "kernels": kernels,

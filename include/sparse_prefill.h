@@ -77,7 +77,7 @@ typedef enum sp_status {
 enum { SP_DTYPE_F32 = 0, SP_DTYPE_BF16 = 1 };
 enum { SP_AGG_MAX = 0, SP_AGG_SUM = 1 };
 enum { SP_OP_DENSE = 0, SP_OP_ORACLE = 1, SP_OP_INDEXER = 2, SP_OP_TOPK = 3,
-       SP_OP_SPARSE = 4, SP_OP_KL = 5, SP_OP_PROJECT = 6 };
+       SP_OP_SPARSE = 4, SP_OP_KL = 5, SP_OP_PROJECT = 6, SP_OP_INDEXER_TOPK = 7 };
 
 /*
  * One GQA layer's sparse-prefill problem (Section 3: S, Hq, Hkv, d_h, the
@@ -163,6 +163,26 @@ int sp_topk_select(const sp_problem *p, const float *scores, int32_t *idx, void 
  */
 int sp_sparse_gqa_attn(const sp_problem *p, const void *q, const void *k, const void *v,
                        const int32_t *idx, void *o, hipStream_t stream);
+
+/*
+ * Fused per-query indexer scoring and top-k (Section 6.3 score equation;
+ * Section 6.4 fused path and Algorithm 2 steps 4-5 with b_sel = 1; Section 4.1
+ * TopK): idx[t,:] = the top-k positions of z[t,s] = ReLU?(index_scale *
+ * <q_idx[t], k_idx[s]>) over s <= t, selected exactly as sp_topk_select does
+ * on those scores (forced window of min(W,k) most recent positions, then
+ * score descending / position ascending; ascending rows, -1 padded), without
+ * storing the S x S score matrix: scores are recomputed on the matrix cores
+ * in each pass of an 8-bit radix select.
+ * Requires block_q = 1, dtype bf16, index_dim 64/128/256, seq_len <= 65535,
+ * index_scale >= 0; otherwise SP_ERR_UNSUPPORTED. q_idx, k_idx: device bf16
+ * [S, d_idx]; idx: device int32 [S, k] (output). workspace: device memory of
+ * at least sp_workspace_bytes(p, SP_OP_INDEXER_TOPK) bytes (about
+ * S * (512 * ceil(S/4096) + 144) bytes), caller-owned, 16-byte aligned,
+ * contents undefined on entry and exit; SP_ERR_WORKSPACE if smaller.
+ * Stream-ordered; several kernels are launched; nothing is allocated.
+ */
+int sp_indexer_topk(const sp_problem *p, const void *q_idx, const void *k_idx, int32_t *idx,
+                    void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Head-collapsed indexer front end (Section 6.3, the projection equations

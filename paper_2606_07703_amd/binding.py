@@ -20,7 +20,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsparse_
 SP_DTYPE = {"f32": 0, "bf16": 1}
 SP_AGG = {"max": 0, "sum": 1}
 SP_OP = {"dense": 0, "oracle": 1, "indexer": 2, "topk": 3, "sparse": 4, "kl": 5,
-         "project": 6}
+         "project": 6, "indexer_topk": 7}
 TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
 STATUS = {0: "SP_OK", -1: "SP_ERR_NULL", -2: "SP_ERR_SHAPE", -3: "SP_ERR_UNSUPPORTED",
           -4: "SP_ERR_WORKSPACE", -5: "SP_ERR_ALIGN", -6: "SP_ERR_NO_DEVICE",
@@ -94,12 +94,13 @@ def load() -> ctypes.CDLL:
         lib.sp_kl_loss.argtypes = [PP, P, ctypes.c_int32, P, P, P, P, P, P]
         I32, F = ctypes.c_int32, ctypes.c_float
         lib.sp_indexer_project.argtypes = [PP, I32, I32, F, F, P, P, P, P, P, P, P, P]
+        lib.sp_indexer_topk.argtypes = [PP, P, P, P, P, ctypes.c_size_t, P]
         lib.sp_workspace_bytes.argtypes = [PP, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
         lib.sp_status_string.argtypes = [ctypes.c_int]
         lib.sp_status_string.restype = ctypes.c_char_p
         lib.sp_version.argtypes = []
         for f in ("sp_dense_attn", "sp_oracle_support", "sp_indexer_scores", "sp_topk_select",
-                  "sp_sparse_gqa_attn", "sp_kl_loss", "sp_indexer_project",
+                  "sp_sparse_gqa_attn", "sp_kl_loss", "sp_indexer_project", "sp_indexer_topk",
                   "sp_workspace_bytes", "sp_version"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
@@ -189,6 +190,25 @@ def sp_sparse_gqa_attn(p: Problem, q, k, v, idx, o, stream=None) -> None:
           _ptr(k, "k", (S, Hkv, d), dt), _ptr(v, "v", (S, Hkv, d), dt),
           _ptr(idx, "idx", (p.num_blocks, p.topk), torch.int32),
           _ptr(o, "o", (S, Hq, d), dt), _stream(stream))
+
+
+def sp_indexer_topk(p: Problem, q_idx, k_idx, idx, workspace=None, stream=None) -> None:
+    """Fused per-query indexer scores and top-k (no S x S score buffer).
+
+    workspace: a device uint8 tensor of at least sp_workspace_bytes(p,
+    "indexer_topk") bytes; when None one is taken from torch's allocator.
+    """
+    S, di = p.seq_len, p.index_dim
+    need = sp_workspace_bytes(p, "indexer_topk")
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q_idx.device)
+    nbytes = workspace.numel() * workspace.element_size()
+    c = p.to_c()
+    bf = torch.bfloat16
+    _call("sp_indexer_topk", ctypes.byref(c), _ptr(q_idx, "q_idx", (S, di), bf),
+          _ptr(k_idx, "k_idx", (S, di), bf), _ptr(idx, "idx", (S, p.topk), torch.int32),
+          _ptr(workspace, "workspace", tuple(workspace.shape), workspace.dtype), nbytes,
+          _stream(stream))
 
 
 def sp_indexer_project(p: Problem, x, w_q, w_k, gamma, beta, q_idx, k_idx, pos0: int = 0,

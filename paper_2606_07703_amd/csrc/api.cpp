@@ -185,6 +185,26 @@ int sp_sparse_gqa_attn(const sp_problem *p, const void *q, const void *k, const 
   return launched(launch_attn_rowwise(r, q, k, v, idx, o, nullptr, stream));
 }
 
+int sp_indexer_topk(const sp_problem *p, const void *q_idx, const void *k_idx, int32_t *idx,
+                    void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  SP_TRY(check_common(p));
+  SP_TRY(check_selection(p));
+  if (p->index_dim != 64 && p->index_dim != 128 && p->index_dim != 256)
+    return SP_ERR_UNSUPPORTED;
+  if (p->relu != 0 && p->relu != 1) return SP_ERR_SHAPE;
+  if (p->block_q != 1) return SP_ERR_UNSUPPORTED;   // the block form aggregates in-kernel
+  if (!q_idx || !k_idx || !idx) return SP_ERR_NULL;
+  if (!aligned16(q_idx) || !aligned16(k_idx) || !aligned16(idx) || !aligned16(workspace))
+    return SP_ERR_ALIGN;
+  const Prob r = resolve(p);
+  if (!indexer_topk_supported(r)) return SP_ERR_UNSUPPORTED;
+  size_t need = 0;
+  SP_TRY(sp_workspace_bytes(p, SP_OP_INDEXER_TOPK, &need));
+  if (!workspace || workspace_bytes < need) return SP_ERR_WORKSPACE;
+  SP_TRY(check_device());
+  return launched(launch_indexer_topk(r, q_idx, k_idx, idx, workspace, stream));
+}
+
 int sp_indexer_project(const sp_problem *p, int32_t d_model, int32_t pos0, float rope_theta,
                        float ln_eps, const void *x, const void *w_q, const void *w_k,
                        const float *gamma, const float *beta, void *q_idx, void *k_idx,
@@ -223,8 +243,12 @@ int sp_kl_loss(const sp_problem *p, const int32_t *rows, int32_t n_rows, const f
 
 int sp_workspace_bytes(const sp_problem *p, int op, size_t *bytes) {
   if (!p || !bytes) return SP_ERR_NULL;
-  if (op < SP_OP_DENSE || op > SP_OP_PROJECT) return SP_ERR_SHAPE;
+  if (op < SP_OP_DENSE || op > SP_OP_INDEXER_TOPK) return SP_ERR_SHAPE;
   *bytes = 0;
+  if (op == SP_OP_INDEXER_TOPK) {
+    SP_TRY(check_common(p));
+    *bytes = indexer_topk_workspace(resolve(p));
+  }
   return SP_OK;
 }
 

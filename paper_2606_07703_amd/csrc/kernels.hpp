@@ -57,6 +57,10 @@ hipError_t launch_indexer_project(int S, int di, int dm, int pos0, float theta, 
                                   const void *x, const void *wq, const void *wk,
                                   const float *gamma, const float *beta, void *qo, void *ko,
                                   hipStream_t st);
+bool indexer_topk_supported(const Prob &p);
+size_t indexer_topk_workspace(const Prob &p);
+hipError_t launch_indexer_topk(const Prob &p, const void *qi, const void *ki, int32_t *idx,
+                               void *ws, hipStream_t st);
 hipError_t launch_kl_loss(int S, int n, const int32_t *rows, const float *P, const float *z,
                           float *kl, float *loss, float *grad, hipStream_t st);
 hipError_t launch_topk(const Prob &p, const float *scores, int32_t *idx, hipStream_t st);

@@ -39,6 +39,7 @@ STAGE_KERNEL_FILE = {
     "perquery.indexer_scores": "indexer_mfma.hip",
     "perquery.topk": "topk.hip",
     "perquery.sparse_attn": "sparse_query_mfma.hip",
+    "perquery.fused_scores_topk": "indexer_topk.hip",
     "dense.attn": "dense_mfma.hip",
     "oracle.normalisers": "dense_mfma.hip",
     "oracle.mass": "mass_mfma.hip",
@@ -48,7 +49,7 @@ STAGE_KERNEL_FILE = {
 }
 STAGES = list(STAGE_KERNEL_FILE)
 # kernel launches per stage when not one (per-row KL, then the mean)
-STAGE_DISPATCHES = {"kl.loss": 2}
+STAGE_DISPATCHES = {"kl.loss": 2, "perquery.fused_scores_topk": 10}
 
 # kernels of the library (everything else in a trace is torch or the runtime)
 LIB_KERNEL_RE = re.compile(r"sp::|_ZN2sp")

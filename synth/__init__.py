@@ -6,5 +6,5 @@ the storage dtype) and the workload shape registry; none of the method's
 arithmetic lives here.
 """
 from .configs import WORKLOADS, Workload, get_workload  # noqa: F401
-from .gen import (make_inputs, make_kl_rows, make_projection_inputs, make_scores,  # noqa: F401
-                  make_support, Inputs)
+from .gen import (make_index_vectors, make_inputs, make_kl_rows, make_projection_inputs,  # noqa: F401
+                  make_scores, make_support, Inputs)

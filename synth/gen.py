@@ -178,3 +178,20 @@ def make_projection_inputs(seq_len: int, d_model: int, index_dim: int, seed: int
     beta = (0.1 * rng.standard_normal(index_dim)).astype(np.float32)
     bf = lambda a: torch.from_numpy(a).to(torch.bfloat16)
     return bf(x), bf(wq), bf(wk), torch.from_numpy(gamma), torch.from_numpy(beta)
+
+
+def make_index_vectors(seq_len: int, index_dim: int, seed: int = 0, kind: str = "gauss"):
+    """Indexer vectors q_idx, k_idx [S, d_idx] in bf16 for exercising the
+    scorer and selection on their own. kind "gauss": N(0,1); "ternary":
+    entries in {-1, 0, 1}, so scores are integers and exact ties are common."""
+    rng = _rng(seed)
+    if kind == "gauss":
+        q = rng.standard_normal((seq_len, index_dim), dtype=np.float32)
+        k = rng.standard_normal((seq_len, index_dim), dtype=np.float32)
+    elif kind == "ternary":
+        q = rng.integers(-1, 2, size=(seq_len, index_dim)).astype(np.float32)
+        k = rng.integers(-1, 2, size=(seq_len, index_dim)).astype(np.float32)
+    else:
+        raise ValueError(kind)
+    bf = lambda a: torch.from_numpy(a).to(torch.bfloat16)
+    return bf(q), bf(k)

@@ -1,7 +1,7 @@
 """GPU parity of the NEXT-row entry points against the fp64 oracle.
 
-KL distillation loss (sp_kl_loss) and the indexer front end
-(sp_indexer_project). Inputs come from the seeded generators only; full-size
+KL distillation loss (sp_kl_loss), the indexer front end
+(sp_indexer_project) and the fused per-query indexer top-k (sp_indexer_topk). Inputs come from the seeded generators only; full-size
 runs are checked on sampled rows.
 """
 import numpy as np
@@ -10,9 +10,9 @@ import torch
 
 import oracle
 from paper_2606_07703_amd import binding as B
-from synth import make_kl_rows, make_projection_inputs
+from synth import make_index_vectors, make_inputs, make_kl_rows, make_projection_inputs
 
-from helpers import say
+from helpers import check_rows_ascending, compare_support, say
 
 pytestmark = pytest.mark.gpu
 
@@ -157,3 +157,61 @@ def test_indexer_project_full_size_sampled():
     rq, rk = oracle.project(x, wq, wk, gamma, beta, rows=sample)
     _check_proj(qo[sample], rq)
     _check_proj(ko[sample], rk)
+
+
+# ------------------------------------------------------- fused indexer top-k
+def _fused_and_unfused(S, di, k, W, relu, qi, ki):
+    p = B.Problem(S, 1, 1, 64, index_dim=di, topk=k, block_q=1, local_window=W, relu=relu)
+    q, kk = qi.cuda(), ki.cuda()
+    fused = torch.full((S, k), -7, dtype=torch.int32, device="cuda")
+    B.sp_indexer_topk(p, q, kk, fused)
+    sc = torch.empty(S, S, device="cuda")
+    B.sp_indexer_scores(p, q, kk, sc)
+    unfused = torch.empty(S, k, dtype=torch.int32, device="cuda")
+    B.sp_topk_select(p, sc, unfused)
+    torch.cuda.synchronize()
+    return fused.cpu().numpy(), unfused.cpu().numpy()
+
+
+FUSED_CASES = [
+    # S, d_idx, k, W, relu, kind
+    (1, 64, 4, 0, 1, "gauss"),
+    (50, 128, 64, 0, 1, "gauss"),        # every row has L <= k
+    (300, 64, 37, 0, 1, "gauss"),
+    (300, 128, 37, 5, 0, "gauss"),
+    (1000, 256, 100, 0, 1, "ternary"),   # integer scores: exact ties everywhere
+    (5000, 128, 512, 0, 1, "gauss"),     # two key chunks
+    (9000, 64, 256, 16, 1, "ternary"),   # three chunks, forced window, ties
+    (700, 128, 700, 3, 1, "gauss"),      # k above every row length but the last
+    (400, 128, 9, 9, 1, "gauss"),        # window takes the whole budget
+]
+
+
+@pytest.mark.parametrize("case", FUSED_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_indexer_topk_fused(case):
+    S, di, k, W, relu, kind = case
+    say(f"fused indexer top-k {case}")
+    qi, ki = make_index_vectors(S, di, seed=S + k, kind=kind)
+    fused, unfused = _fused_and_unfused(S, di, k, W, relu, qi, ki)
+    lens = np.arange(1, S + 1)
+    check_rows_ascending(fused, lens, k)
+    # the same fp32 scores: the fused selection equals the stored-score one
+    assert np.array_equal(fused, unfused)
+    rows = np.unique(np.linspace(0, S - 1, min(S, 64)).round().astype(int))
+    Y = oracle.index_scores(qi, ki, rows=rows, relu=bool(relu))
+    ref = oracle.topk(Y, rows + 1, k, W)
+    for i, t in enumerate(rows):
+        compare_support(fused[t], ref[i], Y[i], t + 1, k, W)
+
+
+def test_indexer_topk_fused_headline_sampled():
+    S, di, k = 32768, 128, 2048
+    say(f"fused indexer top-k S={S} k={k}")
+    inp = make_inputs(S, 32, 8, 128, index_dim=di, dtype="bf16", needles=128, seed=4)
+    fused, unfused = _fused_and_unfused(S, di, k, 0, 1, inp.q_idx, inp.k_idx)
+    assert np.array_equal(fused, unfused)
+    rows = np.array([0, 2046, 2047, 2048, 4095, 4096, 20000, 32767])
+    Y = oracle.index_scores(inp.q_idx, inp.k_idx, rows=rows)
+    ref = oracle.topk(Y, rows + 1, k)
+    for i, t in enumerate(rows):
+        compare_support(fused[t], ref[i], Y[i], t + 1, k)
