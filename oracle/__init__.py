@@ -60,11 +60,12 @@ def _load():
         lib.orc_index_scores.argtypes = [I, I, D, I, P, P, I, P, P]
         lib.orc_block_aggregate.argtypes = [I, I, I, P, P, P]
         lib.orc_topk.argtypes = [I, P, P, ctypes.c_int64, I, I, P]
-        lib.orc_sparse.argtypes = [I, I, I, I, D, P, P, P, I, I, P, I, P, P]
+        lib.orc_sparse.argtypes = [I, I, I, I, D, P, P, P, I, I, P, ctypes.c_int64, I, P, P]
+        lib.orc_mass_heads.argtypes = [I, I, I, I, D, P, P, I, I, I, P, P]
         lib.orc_kl.argtypes = [I, I, P, P, P, P, P]
         lib.orc_project.argtypes = [I, I, I, P, P, P, P, P, D, D, I, I, P, P, P]
         for f in ("orc_dense", "orc_mass", "orc_index_scores", "orc_block_aggregate",
-                  "orc_topk", "orc_sparse", "orc_kl", "orc_project"):
+                  "orc_topk", "orc_sparse", "orc_kl", "orc_project", "orc_mass_heads"):
             getattr(lib, f).restype = None
         _lib = lib
     return _lib
@@ -117,15 +118,24 @@ def dense(q, k, v, rows=None, scale: Optional[float] = None, want_o: bool = True
     return o, lse
 
 
-def mass(q, k, rows=None, scale: Optional[float] = None) -> np.ndarray:
-    """Head-averaged attention mass rows P_t(s) (Section 4.1). Returns [n,S]."""
+def mass(q, k, rows=None, scale: Optional[float] = None, group: Optional[int] = None) -> np.ndarray:
+    """Head-averaged attention mass rows P_t(s) (Section 4.1). Returns [n,S].
+
+    group=None averages over every query head (the token support S_t);
+    group=j over the G heads of KV group j (the per-group support S_{t,j}).
+    """
     q, k = _f64(q), _f64(k)
     S, Hq, d = q.shape
     Hkv = k.shape[1]
     rows = _rows(S, rows)
     scale = 1.0 / np.sqrt(d) if scale is None else scale
     P = np.zeros((len(rows), S))
-    _load().orc_mass(S, Hq, Hkv, d, scale, _ptr(q), _ptr(k), len(rows), _ptr(rows), _ptr(P))
+    if group is None:
+        _load().orc_mass(S, Hq, Hkv, d, scale, _ptr(q), _ptr(k), len(rows), _ptr(rows), _ptr(P))
+    else:
+        G = Hq // Hkv
+        _load().orc_mass_heads(S, Hq, Hkv, d, scale, _ptr(q), _ptr(k), group * G, G, len(rows),
+                               _ptr(rows), _ptr(P))
     return P
 
 
@@ -162,7 +172,11 @@ def topk(Y: np.ndarray, lens, k: int, window: int = 0) -> np.ndarray:
 
 
 def sparse(q, k, v, idx, block_q: int, rows=None, scale: Optional[float] = None) -> np.ndarray:
-    """Restricted attention over shared supports idx [R,kk] (Section 3, 4.2). Returns [n,Hq,d]."""
+    """Restricted attention over supports (Section 3, 4.2). Returns [n,Hq,d].
+
+    idx [R,kk]: one support per selection block shared by every head;
+    idx [Hkv,R,kk]: one support per KV group, used by that group's heads.
+    """
     q, k, v = _f64(q), _f64(k), _f64(v)
     idx = _i32(idx)
     S, Hq, d = q.shape
@@ -170,8 +184,11 @@ def sparse(q, k, v, idx, block_q: int, rows=None, scale: Optional[float] = None)
     rows = _rows(S, rows)
     scale = 1.0 / np.sqrt(d) if scale is None else scale
     o = np.zeros((len(rows), Hq, d))
+    stride = idx.shape[1] * idx.shape[2] if idx.ndim == 3 else 0
+    if idx.ndim == 3:
+        assert idx.shape[0] == Hkv
     _load().orc_sparse(S, Hq, Hkv, d, scale, _ptr(q), _ptr(k), _ptr(v), block_q,
-                       idx.shape[1], _ptr(idx), len(rows), _ptr(rows), _ptr(o))
+                       idx.shape[-1], _ptr(idx), stride, len(rows), _ptr(rows), _ptr(o))
     return o
 
 
@@ -212,10 +229,11 @@ def project(x, wq, wk, gamma, beta, rows=None, pos0: int = 0, theta: float = 100
 # ----------------------------------------------------------------- pipelines
 def support_scores(mode: str, units: Sequence[int], block_q: int, *, q=None, k=None,
                    q_idx=None, k_idx=None, agg: str = "max", attn_scale=None,
-                   index_scale=None, relu: bool = True) -> np.ndarray:
+                   index_scale=None, relu: bool = True, group: Optional[int] = None) -> np.ndarray:
     """Aggregated score rows Y [len(units), S] for selection blocks ``units``.
 
-    mode "oracle": X = head-averaged mass P (Algorithm 1 steps 2-3);
+    mode "oracle": X = head-averaged mass P (Algorithm 1 steps 2-3), over the
+    heads of KV group ``group`` when given (per-group support);
     mode "indexer": X = indexer scores z (Algorithm 2 step 4).
     Then Y = block aggregate of X (identity when block_q == 1).
     """
@@ -224,7 +242,7 @@ def support_scores(mode: str, units: Sequence[int], block_q: int, *, q=None, k=N
     for n, r in enumerate(units):
         trows = block_rows(S, block_q, r)
         if mode == "oracle":
-            X = mass(q, k, trows, attn_scale)
+            X = mass(q, k, trows, attn_scale, group=group)
         elif mode == "indexer":
             X = index_scores(q_idx, k_idx, trows, index_scale, relu)
         else:

@@ -90,10 +90,14 @@ void orc_dense(int S, int Hq, int Hkv, int d, double scale, const double *q,
  *   P_t(s) = (1/Hq) sum_h A[t,h,s],  s <= t.
  * Following Algorithm 1 steps 2-3: the normaliser of every head is computed
  * first, then the probabilities are reconstructed and averaged over heads.
+ * The average runs over the heads [h0, h0 + nh): all Hq heads for the
+ * head-averaged token support S_t, or the G heads of KV group r for the
+ * per-group support S_{t,r} of the head axis (Section 3, support granularity).
  * P is [nrows,S]; entries s > t are written as 0 and carry no meaning.
  */
-void orc_mass(int S, int Hq, int Hkv, int d, double scale, const double *q,
-              const double *k, int nrows, const int32_t *rows, double *P) {
+void orc_mass_heads(int S, int Hq, int Hkv, int d, double scale, const double *q,
+                    const double *k, int h0, int nh, int nrows, const int32_t *rows,
+                    double *P) {
 #pragma omp parallel
   {
     double *l = (double *)malloc(sizeof(double) * (size_t)S);
@@ -102,15 +106,20 @@ void orc_mass(int S, int Hq, int Hkv, int d, double scale, const double *q,
       int t = rows[i];
       double *Pi = P + (size_t)i * S;
       for (int s = 0; s < S; ++s) Pi[s] = 0.0;
-      for (int h = 0; h < Hq; ++h) {
+      for (int h = h0; h < h0 + nh; ++h) {
         logits_row(Hq, Hkv, d, scale, q, k, t, h, l);
         double lz = log_normaliser(l, t + 1);
         for (int s = 0; s <= t; ++s) Pi[s] += exp(l[s] - lz);
       }
-      for (int s = 0; s <= t; ++s) Pi[s] /= (double)Hq;
+      for (int s = 0; s <= t; ++s) Pi[s] /= (double)nh;
     }
     free(l);
   }
+}
+
+void orc_mass(int S, int Hq, int Hkv, int d, double scale, const double *q,
+              const double *k, int nrows, const int32_t *rows, double *P) {
+  orc_mass_heads(S, Hq, Hkv, d, scale, q, k, 0, Hq, nrows, rows, P);
 }
 
 /*
@@ -218,11 +227,13 @@ void orc_topk(int nrows, const int32_t *lens, const double *Y, int64_t ldy, int 
  * r = t / b and uses U = { s in idx[r,:] : 0 <= s <= t, s < S }:
  *   o[t,h] = sum_{s in U} softmax_U(<q_{t,h}, k_{s,g(h)}> * scale)_s v_{s,g(h)}
  * with o = 0 when U is empty. idx is [R,kk]; the order of a row and any
- * sentinel entries do not matter. o is [nrows,Hq,d].
+ * sentinel entries do not matter. o is [nrows,Hq,d]. With per-KV-group
+ * supports S_{t,r} (Section 3, head axis), idx is [Hkv,R,kk] and head h
+ * reads the table of its group g(h): group_stride = R*kk (0 when shared).
  */
 void orc_sparse(int S, int Hq, int Hkv, int d, double scale, const double *q,
                 const double *k, const double *v, int b, int kk, const int32_t *idx,
-                int nrows, const int32_t *rows, double *o) {
+                int64_t group_stride, int nrows, const int32_t *rows, double *o) {
   int G = Hq / Hkv;
 #pragma omp parallel
   {
@@ -232,12 +243,12 @@ void orc_sparse(int S, int Hq, int Hkv, int d, double scale, const double *q,
     for (int i = 0; i < nrows; ++i) {
       int t = rows[i];
       int r = t / b;
-      const int32_t *ir = idx + (size_t)r * kk;
-      int n = 0;
-      for (int c = 0; c < kk; ++c)
-        if (ir[c] >= 0 && ir[c] <= t && ir[c] < S) U[n++] = ir[c];
       for (int h = 0; h < Hq; ++h) {
         int j = h / G;
+        const int32_t *ir = idx + (size_t)j * group_stride + (size_t)r * kk;
+        int n = 0;
+        for (int c = 0; c < kk; ++c)
+          if (ir[c] >= 0 && ir[c] <= t && ir[c] < S) U[n++] = ir[c];
         double *oi = o + ((size_t)i * Hq + h) * d;
         for (int c = 0; c < d; ++c) oi[c] = 0.0;
         if (n == 0) continue;

@@ -1,4 +1,4 @@
-"""Pins for the oracle's KL objective and indexer front end (no GPU).
+"""Pins for the oracle's KL objective, indexer front end and per-group supports (no GPU).
 
 Each check ties the fp64 oracle to something other than itself: scipy's
 relative entropy, closed forms, finite differences, torch's CPU LayerNorm,
@@ -168,3 +168,61 @@ def test_rope_frequency_schedule():
             ang = (3 + t) * 500.0 ** (-2.0 * c / di)
             assert q[t, c] == pytest.approx(np.cos(ang), abs=1e-12)
             assert q[t, c + di // 2] == pytest.approx(np.sin(ang), abs=1e-12)
+
+
+# ------------------------------------------------------ per-KV-group supports
+def _qkv(S, Hq, Hkv, d, seed):
+    rng = np.random.default_rng(seed)
+    return (rng.normal(size=(S, Hq, d)), rng.normal(size=(S, Hkv, d)),
+            rng.normal(size=(S, Hkv, d)))
+
+
+def test_group_mass_of_one_head_is_its_softmax_row():
+    S, H, d = 30, 3, 8
+    q, k, _ = _qkv(S, H, H, d, seed=11)          # G = 1: each group is one head
+    rows = np.array([0, 5, 29])
+    for j in range(H):
+        P = oracle.mass(q, k, rows=rows, group=j)
+        for i, t in enumerate(rows):
+            ref = ssp.softmax(q[t, j] @ k[: t + 1, j].T / np.sqrt(d))
+            assert np.allclose(P[i, : t + 1], ref, rtol=1e-12, atol=1e-15)
+
+
+def test_group_masses_average_to_the_head_averaged_mass():
+    S, Hq, Hkv, d = 40, 8, 4, 16
+    q, k, _ = _qkv(S, Hq, Hkv, d, seed=12)
+    rows = np.arange(0, S, 3)
+    full = oracle.mass(q, k, rows=rows)
+    groups = np.stack([oracle.mass(q, k, rows=rows, group=j) for j in range(Hkv)])
+    assert np.allclose(groups.mean(axis=0), full, rtol=1e-12, atol=1e-15)
+    for i, t in enumerate(rows):
+        assert np.allclose(groups[:, i, : t + 1].sum(axis=1), 1.0, atol=1e-12)
+
+
+def test_per_group_sparse_tables():
+    S, Hq, Hkv, d, b, kk = 48, 6, 3, 8, 4, 9
+    q, k, v = _qkv(S, Hq, Hkv, d, seed=13)
+    rng = np.random.default_rng(14)
+    R = (S + b - 1) // b
+    shared = np.full((R, kk), -1, dtype=np.int32)
+    for r in range(R):
+        t1 = min(r * b + b, S) - 1
+        m = min(kk, t1 + 1)
+        shared[r, :m] = np.sort(rng.choice(t1 + 1, size=m, replace=False))
+    # the same table in every group is the shared-support result
+    same = np.stack([shared] * Hkv)
+    assert np.array_equal(oracle.sparse(q, k, v, same, b), oracle.sparse(q, k, v, shared, b))
+    # a head reads only its own group's table
+    other = same.copy()
+    other[1] = np.roll(shared, 1, axis=1)
+    o1, o0 = oracle.sparse(q, k, v, other, b), oracle.sparse(q, k, v, same, b)
+    G = Hq // Hkv
+    assert np.array_equal(o1[:, :G], o0[:, :G]) and np.array_equal(o1[:, 2 * G:], o0[:, 2 * G:])
+    # full per-group budgets reproduce dense attention (fp64 SDPA)
+    full = np.stack([np.tile(np.arange(S, dtype=np.int32), (R, 1))] * Hkv)
+    qt = torch.from_numpy(q).transpose(0, 1)
+    kt = torch.from_numpy(np.repeat(k, G, axis=1)).transpose(0, 1)
+    vt = torch.from_numpy(np.repeat(v, G, axis=1)).transpose(0, 1)
+    ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, is_causal=True)
+    assert np.allclose(oracle.sparse(q, k, v, full, b), ref.transpose(0, 1).numpy(),
+                       rtol=1e-10, atol=1e-12)
