@@ -33,6 +33,9 @@
  *   idx           [R, k]   int32; ascending positions, then -1 sentinels;
  *                          one row serves every query of block r and every
  *                          KV head
+ * With head_axis = 1 (one support per KV group) mass and idx gain a leading
+ * KV-group axis: mass [Hkv, R, S], idx [Hkv, R, k]; sp_topk_select then
+ * takes scores [Hkv, R, S].
  *
  * Memory and ownership: every pointer is a DEVICE pointer allocated and
  * owned by the caller, 16-byte aligned, and inputs never alias outputs.
@@ -100,6 +103,13 @@ typedef struct sp_problem {
   int32_t dtype;        /* SP_DTYPE_F32 or SP_DTYPE_BF16 for q,k,v,o,q_idx,k_idx */
   float attn_scale;     /* 0 => 1/sqrt(d) (Section 3) */
   float index_scale;    /* 0 => 1/sqrt(d_idx) (Section 6.3) */
+  int32_t head_axis;    /* support granularity on the head axis (Section 3):
+                           0: one head-averaged token support S_t shared by all
+                              query heads (mass and tables [R, ...]);
+                           1: one support S_{t,r} per KV group r, used by the G
+                              query heads of the group (mass and tables
+                              [Hkv, R, ...]). The indexer is head-collapsed and
+                              takes 0 only. */
 } sp_problem;
 
 /*
@@ -121,6 +131,8 @@ int sp_dense_attn(const sp_problem *p, const void *q, const void *k, const void 
  *   mass[r,s] = AGG_{t in block r, t >= s} P_t(s),  s <= t1_r
  * lse must come from sp_dense_attn on the same q, k and problem. AGG is
  * `agg` (the paper's rule is max); with block_q = 1 mass[t,s] = P_t(s).
+ * head_axis = 1: mass[j,r,s] uses P_{t,j}(s) = (1/G) sum over the G heads of
+ * KV group j (the per-group support S_{t,r} of Section 3).
  */
 int sp_oracle_support(const sp_problem *p, const void *q, const void *k, const float *lse,
                       float *mass, hipStream_t stream);
@@ -159,7 +171,8 @@ int sp_topk_select(const sp_problem *p, const float *scores, int32_t *idx, void 
  *   o[t,h] = sum_{s in U} softmax_U(attn_scale * <q[t,h], k[s,g(h)]>)_s v[s,g(h)]
  * and o[t,h] = 0 when U is empty. Entries < 0 or >= S are skipped (they are
  * sentinels); positions within a row must be distinct. The order of a row
- * does not change the result beyond rounding.
+ * does not change the result beyond rounding. head_axis = 1: head h uses the
+ * table idx[g(h), r, :] of its KV group instead.
  */
 int sp_sparse_gqa_attn(const sp_problem *p, const void *q, const void *k, const void *v,
                        const int32_t *idx, void *o, hipStream_t stream);

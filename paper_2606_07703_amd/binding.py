@@ -31,7 +31,8 @@ class SpProblem(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "seq_len", "num_q_heads", "num_kv_heads", "head_dim", "index_dim", "topk", "block_q",
         "causal", "local_window", "agg", "relu", "dtype")] + [
-        ("attn_scale", ctypes.c_float), ("index_scale", ctypes.c_float)]
+        ("attn_scale", ctypes.c_float), ("index_scale", ctypes.c_float),
+        ("head_axis", ctypes.c_int32)]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -51,16 +52,24 @@ class Problem:
     dtype: str = "bf16"
     attn_scale: float = 0.0
     index_scale: float = 0.0
+    head_axis: int = 0    # 1: one support per KV group (tables gain a leading Hkv axis)
 
     @property
     def num_blocks(self) -> int:
         return (self.seq_len + self.block_q - 1) // self.block_q
 
+    @property
+    def table_rows(self) -> tuple:
+        """Leading shape of mass/score and index tables."""
+        R = self.num_blocks
+        return (self.num_kv_heads, R) if self.head_axis else (R,)
+
     def to_c(self) -> SpProblem:
         return SpProblem(self.seq_len, self.num_q_heads, self.num_kv_heads, self.head_dim,
                          self.index_dim, self.topk, self.block_q, self.causal,
                          self.local_window, SP_AGG[self.agg], int(bool(self.relu)),
-                         SP_DTYPE[self.dtype], self.attn_scale, self.index_scale)
+                         SP_DTYPE[self.dtype], self.attn_scale, self.index_scale,
+                         int(self.head_axis))
 
 
 class SparsePrefillError(RuntimeError):
@@ -156,7 +165,7 @@ def sp_oracle_support(p: Problem, q, k, lse, mass, stream=None) -> None:
     c = p.to_c()
     _call("sp_oracle_support", ctypes.byref(c), _ptr(q, "q", (S, Hq, d), dt),
           _ptr(k, "k", (S, Hkv, d), dt), _ptr(lse, "lse", (S, Hq), torch.float32),
-          _ptr(mass, "mass", (p.num_blocks, S), torch.float32), _stream(stream))
+          _ptr(mass, "mass", p.table_rows + (S,), torch.float32), _stream(stream))
 
 
 def sp_indexer_scores(p: Problem, q_idx, k_idx, scores, stream=None) -> None:
@@ -177,8 +186,8 @@ def sp_topk_select(p: Problem, scores, idx, workspace=None, stream=None) -> None
             raise ValueError("workspace must be a contiguous device tensor")
         ws_ptr = workspace.data_ptr()
     _call("sp_topk_select", ctypes.byref(c),
-          _ptr(scores, "scores", (p.num_blocks, p.seq_len), torch.float32),
-          _ptr(idx, "idx", (p.num_blocks, p.topk), torch.int32), ws_ptr, ws_bytes,
+          _ptr(scores, "scores", p.table_rows + (p.seq_len,), torch.float32),
+          _ptr(idx, "idx", p.table_rows + (p.topk,), torch.int32), ws_ptr, ws_bytes,
           _stream(stream))
 
 
@@ -188,7 +197,7 @@ def sp_sparse_gqa_attn(p: Problem, q, k, v, idx, o, stream=None) -> None:
     c = p.to_c()
     _call("sp_sparse_gqa_attn", ctypes.byref(c), _ptr(q, "q", (S, Hq, d), dt),
           _ptr(k, "k", (S, Hkv, d), dt), _ptr(v, "v", (S, Hkv, d), dt),
-          _ptr(idx, "idx", (p.num_blocks, p.topk), torch.int32),
+          _ptr(idx, "idx", p.table_rows + (p.topk,), torch.int32),
           _ptr(o, "o", (S, Hq, d), dt), _stream(stream))
 
 

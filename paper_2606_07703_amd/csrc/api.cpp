@@ -44,6 +44,7 @@ int check_heads(const sp_problem *p) {
 
 int check_selection(const sp_problem *p) {
   if (p->block_q < 1) return SP_ERR_SHAPE;
+  if (p->head_axis != 0 && p->head_axis != 1) return SP_ERR_SHAPE;
   if (p->topk < 1) return SP_ERR_SHAPE;
   if (p->local_window < 0 || p->local_window > p->topk) return SP_ERR_SHAPE;
   return SP_OK;
@@ -69,6 +70,7 @@ Prob resolve(const sp_problem *p) {
   r.agg = p->agg;
   r.relu = p->relu;
   r.dtype = p->dtype;
+  r.ha = p->head_axis;
   r.scale = p->attn_scale != 0.f ? p->attn_scale : 1.f / sqrtf((float)(r.d > 0 ? r.d : 1));
   r.iscale = p->index_scale != 0.f ? p->index_scale : 1.f / sqrtf((float)(r.di > 0 ? r.di : 1));
   return r;
@@ -133,7 +135,8 @@ int sp_oracle_support(const sp_problem *p, const void *q, const void *k, const f
   if (!aligned16(q) || !aligned16(k) || !aligned16(lse) || !aligned16(mass)) return SP_ERR_ALIGN;
   SP_TRY(check_device());
   const Prob r = resolve(p);
-  if (mass_mfma_supported(r)) return launched(launch_mass_mfma(r, q, k, lse, mass, stream));
+  if (!r.ha && mass_mfma_supported(r))
+    return launched(launch_mass_mfma(r, q, k, lse, mass, stream));
   return launched(launch_mass_rowwise(r, q, k, lse, mass, stream));
 }
 
@@ -141,6 +144,7 @@ int sp_indexer_scores(const sp_problem *p, const void *q_idx, const void *k_idx,
                       hipStream_t stream) {
   SP_TRY(check_common(p));
   SP_TRY(check_selection(p));
+  if (p->head_axis != 0) return SP_ERR_UNSUPPORTED;   // the indexer is head-collapsed
   SP_TRY(check_agg(p));
   if (p->index_dim != 64 && p->index_dim != 128 && p->index_dim != 256)
     return SP_ERR_UNSUPPORTED;
@@ -189,6 +193,7 @@ int sp_indexer_topk(const sp_problem *p, const void *q_idx, const void *k_idx, i
                     void *workspace, size_t workspace_bytes, hipStream_t stream) {
   SP_TRY(check_common(p));
   SP_TRY(check_selection(p));
+  if (p->head_axis != 0) return SP_ERR_UNSUPPORTED;   // the indexer is head-collapsed
   if (p->index_dim != 64 && p->index_dim != 128 && p->index_dim != 256)
     return SP_ERR_UNSUPPORTED;
   if (p->relu != 0 && p->relu != 1) return SP_ERR_SHAPE;

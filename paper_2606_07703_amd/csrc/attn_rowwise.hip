@@ -28,7 +28,7 @@ template <typename T, int D, int HPW, bool SPARSE>
 __global__ __launch_bounds__(64) void attn_rowwise_kernel(
     int S, int Hq, int Hkv, int G, float scale_log2, const T *__restrict__ q,
     const T *__restrict__ k, const T *__restrict__ v, const int32_t *__restrict__ idx, int kk,
-    int b, T *__restrict__ o, float *__restrict__ lse) {
+    int b, size_t gstride, T *__restrict__ o, float *__restrict__ lse) {
   constexpr int EPL = D / 16;
   const int t = blockIdx.x;
   const int h0 = blockIdx.y * HPW;
@@ -54,7 +54,7 @@ __global__ __launch_bounds__(64) void attn_rowwise_kernel(
   }
 
   const int n = SPARSE ? kk : t + 1;
-  const int32_t *ir = SPARSE ? idx + (size_t)(t / b) * kk : nullptr;
+  const int32_t *ir = SPARSE ? idx + (size_t)j * gstride + (size_t)(t / b) * kk : nullptr;
   for (int base = 0; base < n; base += 4) {
     const int i = base + grp;
     int s = i;
@@ -132,11 +132,11 @@ hipError_t launch_t(const Prob &p, const void *q, const void *k, const void *v,
   if (idx)
     hipLaunchKernelGGL((attn_rowwise_kernel<T, D, HPW, true>), grid, dim3(64), 0, st, p.S,
                        p.Hq, p.Hkv, p.G, sl2, (const T *)q, (const T *)k, (const T *)v, idx,
-                       p.k, p.b, (T *)o, lse);
+                       p.k, p.b, p.idx_group_stride(), (T *)o, lse);
   else
     hipLaunchKernelGGL((attn_rowwise_kernel<T, D, HPW, false>), grid, dim3(64), 0, st, p.S,
                        p.Hq, p.Hkv, p.G, sl2, (const T *)q, (const T *)k, (const T *)v,
-                       nullptr, 0, 1, (T *)o, lse);
+                       nullptr, 0, 1, (size_t)0, (T *)o, lse);
   return hipGetLastError();
 }
 

@@ -12,8 +12,11 @@ namespace sp {
 // A validated problem with defaults resolved.
 struct Prob {
   int S, Hq, Hkv, G, d, di, k, b, R, W, agg, relu, dtype;
+  int ha;        // head axis: 0 one support shared by all heads, 1 one per KV group
   float scale;   // attention logit scale
   float iscale;  // indexer score scale
+  // elements between the support tables of consecutive KV groups
+  size_t idx_group_stride() const { return ha ? (size_t)R * k : 0; }
 };
 
 // Dense (idx == nullptr) or sparse (idx != nullptr) attention, one wave per

@@ -21,7 +21,7 @@ constexpr int kMaxSupport = 4096;   // support row cached in LDS
 
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
-    int S, int Hq, int Hkv, int G, int b, int kk, float scale_log2,
+    int S, int Hq, int Hkv, int G, int b, int kk, size_t gstride, float scale_log2,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const int32_t *__restrict__ idx,
     uint16_t *__restrict__ o) {
@@ -43,7 +43,7 @@ __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
   // block can use (any order).
   int last = -1;
   for (int c = tid; c < kk; c += NT) {
-    const int s = idx[(size_t)r * kk + c];
+    const int s = idx[(size_t)j * gstride + (size_t)r * kk + c];
     ir[c] = s;
     if (s >= 0 && s <= t1) last = c;
   }
@@ -96,7 +96,8 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
   const float sl2 = p.scale * kLog2e;
 #define SP_SB(NW)                                                                            \
   hipLaunchKernelGGL((sparse_block_kernel<D, NW>), grid, dim3(NW * 64), 0, st, p.S, p.Hq,    \
-                     p.Hkv, p.G, p.b, p.k, sl2, (const uint16_t *)q, (const uint16_t *)k,     \
+                     p.Hkv, p.G, p.b, p.k, p.idx_group_stride(), sl2, (const uint16_t *)q,      \
+                     (const uint16_t *)k,                                                     \
                      (const uint16_t *)v, idx, (uint16_t *)o)
   switch (nw) {
     case 1: SP_SB(1); break;

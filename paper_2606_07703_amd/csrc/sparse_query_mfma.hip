@@ -56,7 +56,7 @@ __device__ __forceinline__ float reduce4(float x, Op op) {
 
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
-    int S, int Hq, int Hkv, int G, int b, int kk, int n_groups, float scale_log2,
+    int S, int Hq, int Hkv, int G, int b, int kk, size_t gstride, int n_groups, float scale_log2,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const int32_t *__restrict__ idx,
     uint16_t *__restrict__ o) {
@@ -75,7 +75,7 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
   const int grp = n_groups - 1 - blockIdx.x / Hkv;   // longest queries first
   const int t = grp * NW + wave;
   if (t >= S) return;   // no workgroup barrier below: waves are independent
-  const int32_t *row = idx + (size_t)(t / b) * kk;
+  const int32_t *row = idx + (size_t)j * gstride + (size_t)(t / b) * kk;
   int *ipos = sh.pos[wave];
   char *vb = sh.vbuf[wave];
 
@@ -227,7 +227,8 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
   constexpr int NW = 4;
   const int n_groups = (p.S + NW - 1) / NW;
   hipLaunchKernelGGL((sparse_query_kernel<D, NW>), dim3(n_groups * p.Hkv), dim3(NW * 64), 0, st,
-                     p.S, p.Hq, p.Hkv, p.G, p.b, p.k, n_groups, p.scale * kLog2e,
+                     p.S, p.Hq, p.Hkv, p.G, p.b, p.k, p.idx_group_stride(), n_groups,
+                     p.scale * kLog2e,
                      (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, idx,
                      (uint16_t *)o);
   return hipGetLastError();

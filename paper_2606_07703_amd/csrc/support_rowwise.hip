@@ -3,6 +3,8 @@
 //
 // Oracle mass (Section 4.1, 4.2; Algorithm 1 step 3):
 //   P_t(s) = (1/Hq) sum_h exp(scale <q[t,h],k[s,g(h)]> - lse[t,h]),  s <= t
+// or, for the per-KV-group support of the head axis (Section 3), the same
+// average over the G heads of one KV group, one table per group.
 // Indexer score (Section 6.3; Algorithm 2 step 4):
 //   z[t,s] = ReLU(iscale <q_idx[t], k_idx[s]>),  s <= t
 // Block aggregate (Section 4.2): Y[r,s] = AGG_{t in block r, t >= s} X[t,s].
@@ -23,8 +25,9 @@ constexpr int kCols = 256;
 
 template <typename T, int D>
 __global__ __launch_bounds__(kCols) void mass_rowwise_kernel(
-    int S, int Hq, int Hkv, int G, int b, int agg, float scale_log2, const T *__restrict__ q,
-    const T *__restrict__ k, const float *__restrict__ lse, float *__restrict__ mass) {
+    int S, int Hq, int Hkv, int G, int b, int agg, int per_group, float scale_log2,
+    const T *__restrict__ q, const T *__restrict__ k, const float *__restrict__ lse,
+    float *__restrict__ mass) {
   extern __shared__ float smem[];
   float *qs = smem;            // [Hq, D], pre-scaled by scale*log2(e)
   float *ls = smem + Hq * D;   // [Hq], lse*log2(e)
@@ -34,7 +37,10 @@ __global__ __launch_bounds__(kCols) void mass_rowwise_kernel(
   const int c0 = blockIdx.y * kCols;
   if (c0 > t1) return;  // uniform over the workgroup
   const int s = c0 + threadIdx.x;
-  const float invH = 1.f / (float)Hq;
+  // KV groups averaged: all of them, or group blockIdx.z (per-group support)
+  const int j0 = per_group ? (int)blockIdx.z : 0, nj = per_group ? 1 : Hkv;
+  mass += (size_t)blockIdx.z * gridDim.x * S;
+  const float invH = 1.f / (float)(nj * G);
   float y = 0.f;
   bool have = false;
   for (int t = t0; t <= t1; ++t) {
@@ -45,7 +51,7 @@ __global__ __launch_bounds__(kCols) void mass_rowwise_kernel(
     __syncthreads();
     if (s <= t) {
       float pt = 0.f;
-      for (int j = 0; j < Hkv; ++j) {
+      for (int j = j0; j < j0 + nj; ++j) {
         float kr[D];
         load_row<D>(k + ((size_t)s * Hkv + j) * D, kr);
         for (int hh = 0; hh < G; ++hh) {
@@ -118,10 +124,11 @@ hipError_t launch_mass_rowwise(const Prob &p, const void *q, const void *k, cons
                                float *mass, hipStream_t st) {
   const size_t lds = sizeof(float) * (size_t)p.Hq * (p.d + 1);
   const float sl2 = p.scale * kLog2e;
-  const dim3 grid = grid_for(p);
+  dim3 grid = grid_for(p);
+  grid.z = p.ha ? p.Hkv : 1;   // per-group support: one mass table per KV group
 #define SP_MASS(T, D)                                                                        \
   hipLaunchKernelGGL((mass_rowwise_kernel<T, D>), grid, dim3(kCols), lds, st, p.S, p.Hq,    \
-                     p.Hkv, p.G, p.b, p.agg, sl2, (const T *)q, (const T *)k, lse, mass)
+                     p.Hkv, p.G, p.b, p.agg, p.ha, sl2, (const T *)q, (const T *)k, lse, mass)
   if (p.dtype == SP_DTYPE_BF16) {
     if (p.d == 64) SP_MASS(bf16, 64); else SP_MASS(bf16, 128);
   } else {

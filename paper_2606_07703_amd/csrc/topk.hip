@@ -76,8 +76,10 @@ __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int b, int k, i
   const int tid = threadIdx.x, lane = tid & 63;
   const int t1 = min(r * b + b, S) - 1;
   const int L = t1 + 1;
-  int32_t *out = idx + (size_t)r * k;
-  const float *row = scores + (size_t)r * S;
+  // blockIdx.y: the KV group of a per-group table (0 for a shared one)
+  const size_t row_id = (size_t)blockIdx.y * gridDim.x + r;
+  int32_t *out = idx + row_id * k;
+  const float *row = scores + row_id * S;
   if (L <= k) {
     for (int c = tid; c < k; c += NT) out[c] = c < L ? c : -1;
     return;
@@ -86,7 +88,7 @@ __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int b, int k, i
   const int nc = L - Wf;
   const int kp = k - Wf;
   const int nsub = (nc + NT * kRun - 1) / (NT * kRun);   // runs in use (<= kRegSub)
-  const bool vec = ((((size_t)r * S) & 3) == 0);         // row start 16-byte aligned
+  const bool vec = (((row_id * S) & 3) == 0);            // row start 16-byte aligned
 
   // Run j of thread t covers positions [kRun*(t + NT*j), +kRun).
   uint32_t key[kRegSub][kRun];
@@ -209,8 +211,10 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int b, int k, int
   const int tid = threadIdx.x, lane = tid & 63;
   const int t1 = min(r * b + b, S) - 1;
   const int L = t1 + 1;
-  int32_t *out = idx + (size_t)r * k;
-  const float *row = scores + (size_t)r * S;
+  // blockIdx.y: the KV group of a per-group table (0 for a shared one)
+  const size_t row_id = (size_t)blockIdx.y * gridDim.x + r;
+  int32_t *out = idx + row_id * k;
+  const float *row = scores + row_id * S;
 
   if (L <= k) {
     for (int c = tid; c < k; c += kNT) out[c] = c < L ? c : -1;
@@ -306,11 +310,11 @@ hipError_t launch_topk(const Prob &p, const float *scores, int32_t *idx, hipStre
   const int Lmax = min(p.R * p.b, p.S);
   const int ncmax = Lmax - min(p.W, p.k);
   if (ncmax <= kRegCap)
-    hipLaunchKernelGGL(topk_reg_kernel, dim3(p.R), dim3(kRegNT), 0, st, p.S, p.b, p.k, p.W,
-                       scores, idx);
+    hipLaunchKernelGGL(topk_reg_kernel, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kRegNT), 0, st, p.S,
+                       p.b, p.k, p.W, scores, idx);
   else
-    hipLaunchKernelGGL(topk_rows_kernel, dim3(p.R), dim3(kNT), 0, st, p.S, p.b, p.k, p.W,
-                       scores, idx);
+    hipLaunchKernelGGL(topk_rows_kernel, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kNT), 0, st, p.S,
+                       p.b, p.k, p.W, scores, idx);
   return hipGetLastError();
 }
 

@@ -31,8 +31,8 @@ class Buffers:
     def for_problem(p: Problem, device="cuda", oracle: bool = False) -> "Buffers":
         dt = TORCH_DTYPE[p.dtype]
         o = torch.empty(p.seq_len, p.num_q_heads, p.head_dim, dtype=dt, device=device)
-        scores = torch.empty(p.num_blocks, p.seq_len, dtype=torch.float32, device=device)
-        idx = torch.empty(p.num_blocks, p.topk, dtype=torch.int32, device=device)
+        scores = torch.empty(p.table_rows + (p.seq_len,), dtype=torch.float32, device=device)
+        idx = torch.empty(p.table_rows + (p.topk,), dtype=torch.int32, device=device)
         lse = (torch.empty(p.seq_len, p.num_q_heads, dtype=torch.float32, device=device)
                if oracle else None)
         return Buffers(o=o, scores=scores, idx=idx, lse=lse)

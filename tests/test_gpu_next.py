@@ -215,3 +215,64 @@ def test_indexer_topk_fused_headline_sampled():
     ref = oracle.topk(Y, rows + 1, k)
     for i, t in enumerate(rows):
         compare_support(fused[t], ref[i], Y[i], t + 1, k)
+
+
+# ------------------------------------------------- per-KV-group supports (f3)
+from synth import make_support  # noqa: E402
+from helpers import max_err, tol_for  # noqa: E402
+
+
+@pytest.mark.parametrize("S,Hq,Hkv,d,b,dtype", [(200, 8, 2, 64, 1, "f32"),
+                                                (300, 8, 2, 128, 16, "bf16"),
+                                                (257, 12, 3, 64, 4, "bf16")])
+def test_group_mass_and_topk(S, Hq, Hkv, d, b, dtype):
+    say(f"per-group mass+topk S={S} Hq={Hq} Hkv={Hkv} d={d} b={b} {dtype}")
+    k = 24
+    inp = make_inputs(S, Hq, Hkv, d, dtype=dtype, seed=S + b, peaked=True, needles=4)
+    p = B.Problem(S, Hq, Hkv, d, topk=k, block_q=b, dtype=dtype, head_axis=1, local_window=2)
+    q, kk, v = inp.q.cuda(), inp.k.cuda(), inp.v.cuda()
+    lse = torch.empty(S, Hq, device="cuda")
+    B.sp_dense_attn(p, q, kk, v, None, lse)
+    R = p.num_blocks
+    mass = torch.full((Hkv, R, S), float("nan"), device="cuda")
+    B.sp_oracle_support(p, q, kk, lse, mass)
+    idx = torch.empty(Hkv, R, k, dtype=torch.int32, device="cuda")
+    B.sp_topk_select(p, mass, idx)
+    torch.cuda.synchronize()
+    got, gidx = mass.cpu().double().numpy(), idx.cpu().numpy()
+    lens = np.array([min(r * b + b, S) for r in range(R)])
+    for j in range(Hkv):
+        ref = oracle.support_scores("oracle", range(R), b, q=inp.q, k=inp.k, group=j)
+        ref_idx = oracle.topk(ref, lens, k, 2)
+        check_rows_ascending(gidx[j], lens, k)
+        for r in range(R):
+            L = lens[r]
+            assert max_err(got[j, r, :L], ref[r, :L]) <= 1e-4 * np.abs(ref[r, :L]).max()
+            assert np.all(np.isnan(got[j, r, L:]))
+            compare_support(gidx[j, r], ref_idx[r], ref[r], L, k, 2)
+
+
+@pytest.mark.parametrize("S,Hq,Hkv,d,b,dtype", [(300, 8, 2, 128, 64, "bf16"),
+                                                (300, 8, 2, 64, 16, "bf16"),
+                                                (257, 8, 4, 128, 1, "bf16"),
+                                                (200, 6, 3, 64, 3, "bf16"),
+                                                (150, 4, 2, 64, 8, "f32")])
+def test_group_sparse_attention(S, Hq, Hkv, d, b, dtype):
+    say(f"per-group sparse S={S} Hq={Hq} Hkv={Hkv} d={d} b={b} {dtype}")
+    k = 40
+    inp = make_inputs(S, Hq, Hkv, d, dtype=dtype, seed=S + d, peaked=True)
+    tables = torch.stack([make_support(S, b, k, seed=10 + j, shuffle=j % 2 == 1)
+                          for j in range(Hkv)])
+    p = B.Problem(S, Hq, Hkv, d, topk=k, block_q=b, dtype=dtype, head_axis=1)
+    o = torch.empty(S, Hq, d, dtype=inp.q.dtype, device="cuda")
+    B.sp_sparse_gqa_attn(p, inp.q.cuda(), inp.k.cuda(), inp.v.cuda(), tables.cuda(), o)
+    torch.cuda.synchronize()
+    ref = oracle.sparse(inp.q, inp.k, inp.v, tables, b)
+    assert max_err(o.cpu().double().numpy(), ref) <= tol_for(dtype)
+
+
+def test_indexer_rejects_per_group_supports():
+    p = B.Problem(64, 8, 2, 64, index_dim=64, topk=8, head_axis=1)
+    x = torch.zeros(64, 64, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(B.SparsePrefillError):
+        B.sp_indexer_scores(p, x, x, torch.empty(64, 64, device="cuda"))
