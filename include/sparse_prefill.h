@@ -178,6 +178,24 @@ int sp_sparse_gqa_attn(const sp_problem *p, const void *q, const void *k, const 
                        const int32_t *idx, void *o, hipStream_t stream);
 
 /*
+ * Sparse GQA attention reading K and V from a paged cache (Section 6.4: the
+ * serving path gathers the selected support inside the attention kernel, from
+ * a paged KV cache). Same result as sp_sparse_gqa_attn on the contiguous K, V
+ * with K[s] = k_pages[page_table[s / page_size], s % page_size]:
+ *   k_pages, v_pages: device [num_pages, page_size, Hkv, d] (problem dtype),
+ *                     each below 4 GiB;
+ *   page_table:       device int32 [ceil(S / page_size)]: the physical page of
+ *                     each logical page of the sequence. A selected position
+ *                     whose page entry is outside [0, num_pages) is skipped
+ *                     like a sentinel (nothing outside the cache is read).
+ * Everything else (q, idx, o, head_axis, block_q) as sp_sparse_gqa_attn.
+ */
+int sp_sparse_gqa_attn_paged(const sp_problem *p, const void *q, const void *k_pages,
+                             const void *v_pages, const int32_t *page_table, int32_t page_size,
+                             int32_t num_pages, const int32_t *idx, void *o,
+                             hipStream_t stream);
+
+/*
  * Fused per-query indexer scoring and top-k (Section 6.3 score equation;
  * Section 6.4 fused path and Algorithm 2 steps 4-5 with b_sel = 1; Section 4.1
  * TopK): idx[t,:] = the top-k positions of z[t,s] = ReLU?(index_scale *

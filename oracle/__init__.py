@@ -192,6 +192,32 @@ def sparse(q, k, v, idx, block_q: int, rows=None, scale: Optional[float] = None)
     return o
 
 
+def sparse_paged(q, k_pages, v_pages, page_table, idx, block_q: int, rows=None,
+                 scale: Optional[float] = None) -> np.ndarray:
+    """Restricted attention with K/V in a paged cache (Section 6.4).
+
+    Token s is row s % page_size of page page_table[s // page_size]; a
+    selected position whose page entry lies outside the cache contributes
+    nothing (it becomes a sentinel). The attention itself is ``sparse``.
+    """
+    kp, vp = _f64(k_pages), _f64(v_pages)
+    table = _i32(page_table)
+    idx = _i32(idx).copy()
+    npg, ps = kp.shape[0], kp.shape[1]
+    S = _f64(q).shape[0]
+    k = np.zeros((S,) + kp.shape[2:])
+    v = np.zeros((S,) + vp.shape[2:])
+    ok = np.zeros(S, dtype=bool)
+    for s in range(S):
+        pg = table[s // ps]
+        if 0 <= pg < npg:
+            k[s], v[s], ok[s] = kp[pg, s % ps], vp[pg, s % ps], True
+    valid = (idx >= 0) & (idx < S)
+    bad = valid & ~ok[np.clip(idx, 0, S - 1)]
+    idx[bad] = -1
+    return sparse(q, k, v, idx, block_q, rows=rows, scale=scale)
+
+
 def kl(P, z, rows):
     """KL(P_i || softmax(z_i)) over s <= rows[i] (Section 6.2).
 

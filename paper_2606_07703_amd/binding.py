@@ -104,12 +104,14 @@ def load() -> ctypes.CDLL:
         I32, F = ctypes.c_int32, ctypes.c_float
         lib.sp_indexer_project.argtypes = [PP, I32, I32, F, F, P, P, P, P, P, P, P, P]
         lib.sp_indexer_topk.argtypes = [PP, P, P, P, P, ctypes.c_size_t, P]
+        lib.sp_sparse_gqa_attn_paged.argtypes = [PP, P, P, P, P, I32, I32, P, P, P]
         lib.sp_workspace_bytes.argtypes = [PP, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
         lib.sp_status_string.argtypes = [ctypes.c_int]
         lib.sp_status_string.restype = ctypes.c_char_p
         lib.sp_version.argtypes = []
         for f in ("sp_dense_attn", "sp_oracle_support", "sp_indexer_scores", "sp_topk_select",
                   "sp_sparse_gqa_attn", "sp_kl_loss", "sp_indexer_project", "sp_indexer_topk",
+                  "sp_sparse_gqa_attn_paged",
                   "sp_workspace_bytes", "sp_version"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
@@ -243,6 +245,21 @@ def sp_kl_loss(p: Problem, rows, P, z, kl=None, loss=None, grad_z=None, stream=N
           _ptr(P, "P", (n, S), torch.float32), _ptr(z, "z", (n, S), torch.float32),
           _ptr(kl, "kl", (n,), torch.float32), _ptr(loss, "loss", (1,), torch.float32),
           _ptr(grad_z, "grad_z", (n, S), torch.float32), _stream(stream))
+
+
+def sp_sparse_gqa_attn_paged(p: Problem, q, k_pages, v_pages, page_table, idx, o,
+                             stream=None) -> None:
+    """Sparse GQA attention with K/V in a paged cache [num_pages, page_size, Hkv, d]."""
+    S, Hq, Hkv, d = p.seq_len, p.num_q_heads, p.num_kv_heads, p.head_dim
+    dt = TORCH_DTYPE[p.dtype]
+    npg, ps = (k_pages.shape[0], k_pages.shape[1]) if k_pages is not None else (0, 0)
+    c = p.to_c()
+    _call("sp_sparse_gqa_attn_paged", ctypes.byref(c), _ptr(q, "q", (S, Hq, d), dt),
+          _ptr(k_pages, "k_pages", (npg, ps, Hkv, d), dt),
+          _ptr(v_pages, "v_pages", (npg, ps, Hkv, d), dt),
+          _ptr(page_table, "page_table", ((S + ps - 1) // max(ps, 1),), torch.int32), ps, npg,
+          _ptr(idx, "idx", p.table_rows + (p.topk,), torch.int32),
+          _ptr(o, "o", (S, Hq, d), dt), _stream(stream))
 
 
 def sp_workspace_bytes(p: Problem, op: str) -> int:

@@ -246,6 +246,34 @@ int sp_kl_loss(const sp_problem *p, const int32_t *rows, int32_t n_rows, const f
   return launched(launch_kl_loss(p->seq_len, n_rows, rows, P, z, kl, loss, grad_z, stream));
 }
 
+int sp_sparse_gqa_attn_paged(const sp_problem *p, const void *q, const void *k_pages,
+                             const void *v_pages, const int32_t *page_table, int32_t page_size,
+                             int32_t num_pages, const int32_t *idx, void *o,
+                             hipStream_t stream) {
+  SP_TRY(check_common(p));
+  SP_TRY(check_heads(p));
+  SP_TRY(check_selection(p));
+  if (page_size < 1 || num_pages < 1) return SP_ERR_SHAPE;
+  const int64_t elt = p->dtype == SP_DTYPE_BF16 ? 2 : 4;
+  if ((int64_t)num_pages * page_size * p->num_kv_heads * p->head_dim * elt >= (int64_t(1) << 32))
+    return SP_ERR_UNSUPPORTED;
+  if (!q || !k_pages || !v_pages || !page_table || !idx || !o) return SP_ERR_NULL;
+  if (!aligned16(q) || !aligned16(k_pages) || !aligned16(v_pages) || !aligned16(page_table) ||
+      !aligned16(idx) || !aligned16(o))
+    return SP_ERR_ALIGN;
+  SP_TRY(check_device());
+  const Prob r = resolve(p);
+  KvPages pages;
+  pages.table = page_table;
+  pages.page_size = page_size;
+  pages.num_pages = num_pages;
+  if (sparse_block_mfma_supported(r))
+    return launched(launch_sparse_block_mfma(r, q, k_pages, v_pages, idx, o, stream, pages));
+  if (sparse_query_mfma_supported(r))
+    return launched(launch_sparse_query_mfma(r, q, k_pages, v_pages, idx, o, stream, pages));
+  return launched(launch_attn_rowwise(r, q, k_pages, v_pages, idx, o, nullptr, stream, pages));
+}
+
 int sp_workspace_bytes(const sp_problem *p, int op, size_t *bytes) {
   if (!p || !bytes) return SP_ERR_NULL;
   if (op < SP_OP_DENSE || op > SP_OP_INDEXER_TOPK) return SP_ERR_SHAPE;

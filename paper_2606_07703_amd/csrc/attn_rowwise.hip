@@ -28,7 +28,7 @@ template <typename T, int D, int HPW, bool SPARSE>
 __global__ __launch_bounds__(64) void attn_rowwise_kernel(
     int S, int Hq, int Hkv, int G, float scale_log2, const T *__restrict__ q,
     const T *__restrict__ k, const T *__restrict__ v, const int32_t *__restrict__ idx, int kk,
-    int b, size_t gstride, T *__restrict__ o, float *__restrict__ lse) {
+    int b, size_t gstride, T *__restrict__ o, float *__restrict__ lse, KvPages pages) {
   constexpr int EPL = D / 16;
   const int t = blockIdx.x;
   const int h0 = blockIdx.y * HPW;
@@ -62,6 +62,10 @@ __global__ __launch_bounds__(64) void attn_rowwise_kernel(
     if (SPARSE) {
       s = valid ? ir[i] : -1;
       valid = valid && s >= 0 && s <= t && s < S;
+      if (valid) {
+        s = pages.row(s);   // the K/V row (identity unless the cache is paged)
+        valid = s >= 0;
+      }
     }
     if (!valid) s = 0;
     float kf[EPL], vf[EPL];
@@ -126,38 +130,39 @@ __global__ __launch_bounds__(64) void attn_rowwise_kernel(
 
 template <typename T, int D, int HPW>
 hipError_t launch_t(const Prob &p, const void *q, const void *k, const void *v,
-                    const int32_t *idx, void *o, float *lse, hipStream_t st) {
+                    const int32_t *idx, void *o, float *lse, hipStream_t st, KvPages pages) {
   dim3 grid(p.S, p.Hq / HPW);
   const float sl2 = p.scale * kLog2e;
   if (idx)
     hipLaunchKernelGGL((attn_rowwise_kernel<T, D, HPW, true>), grid, dim3(64), 0, st, p.S,
                        p.Hq, p.Hkv, p.G, sl2, (const T *)q, (const T *)k, (const T *)v, idx,
-                       p.k, p.b, p.idx_group_stride(), (T *)o, lse);
+                       p.k, p.b, p.idx_group_stride(), (T *)o, lse, pages);
   else
     hipLaunchKernelGGL((attn_rowwise_kernel<T, D, HPW, false>), grid, dim3(64), 0, st, p.S,
                        p.Hq, p.Hkv, p.G, sl2, (const T *)q, (const T *)k, (const T *)v,
-                       nullptr, 0, 1, (size_t)0, (T *)o, lse);
+                       nullptr, 0, 1, (size_t)0, (T *)o, lse, KvPages());
   return hipGetLastError();
 }
 
 template <typename T, int D>
 hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
-                    const int32_t *idx, void *o, float *lse, hipStream_t st) {
-  if (p.G % 4 == 0) return launch_t<T, D, 4>(p, q, k, v, idx, o, lse, st);
-  if (p.G % 2 == 0) return launch_t<T, D, 2>(p, q, k, v, idx, o, lse, st);
-  return launch_t<T, D, 1>(p, q, k, v, idx, o, lse, st);
+                    const int32_t *idx, void *o, float *lse, hipStream_t st, KvPages pages) {
+  if (p.G % 4 == 0) return launch_t<T, D, 4>(p, q, k, v, idx, o, lse, st, pages);
+  if (p.G % 2 == 0) return launch_t<T, D, 2>(p, q, k, v, idx, o, lse, st, pages);
+  return launch_t<T, D, 1>(p, q, k, v, idx, o, lse, st, pages);
 }
 
 }  // namespace
 
 hipError_t launch_attn_rowwise(const Prob &p, const void *q, const void *k, const void *v,
-                               const int32_t *idx, void *o, float *lse, hipStream_t st) {
+                               const int32_t *idx, void *o, float *lse, hipStream_t st,
+                               KvPages pages) {
   if (p.dtype == SP_DTYPE_BF16) {
-    if (p.d == 64) return launch_d<bf16, 64>(p, q, k, v, idx, o, lse, st);
-    return launch_d<bf16, 128>(p, q, k, v, idx, o, lse, st);
+    if (p.d == 64) return launch_d<bf16, 64>(p, q, k, v, idx, o, lse, st, pages);
+    return launch_d<bf16, 128>(p, q, k, v, idx, o, lse, st, pages);
   }
-  if (p.d == 64) return launch_d<float, 64>(p, q, k, v, idx, o, lse, st);
-  return launch_d<float, 128>(p, q, k, v, idx, o, lse, st);
+  if (p.d == 64) return launch_d<float, 64>(p, q, k, v, idx, o, lse, st, pages);
+  return launch_d<float, 128>(p, q, k, v, idx, o, lse, st, pages);
 }
 
 }  // namespace sp

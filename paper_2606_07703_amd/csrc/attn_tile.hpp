@@ -75,10 +75,20 @@ struct KVStage {
   __device__ __forceinline__ void load(const uint16_t *__restrict__ k,
                                        const uint16_t *__restrict__ v, int S, int Hkv, int j,
                                        int tid, POS pos) {
+    load_rows(k, v, S, Hkv, j, tid, pos, pos);
+  }
+
+  // As load, with the K/V row of tile entry e given by row(e) (a paged
+  // cache) while pos(e) stays the token position the mask uses; k and v
+  // hold nrows rows of Hkv heads.
+  template <typename POS, typename ROW>
+  __device__ __forceinline__ void load_rows(const uint16_t *__restrict__ k,
+                                            const uint16_t *__restrict__ v, int nrows, int Hkv,
+                                            int j, int tid, POS pos, ROW row) {
     // Rows are fetched through buffer resources (base and size in SGPRs,
     // 32-bit byte offsets per lane): one multiply-add per piece instead of
     // 64-bit address arithmetic. The API keeps k and v below 4 GiB.
-    const uint32_t nbytes = (uint32_t)S * Hkv * D * 2;
+    const uint32_t nbytes = (uint32_t)nrows * Hkv * D * 2;
     const auto krs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(k), (short)0,
                                                        nbytes, kBufferDword3);
     const auto vrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(v), (short)0,
@@ -88,8 +98,8 @@ struct KVStage {
     for (int i = 0; i < PER; ++i) {
       const int c = tid + i * NT;
       const int key = c / (D / 8), col = c % (D / 8);
-      int s = c < PIECES ? pos(key) : 0;
-      s = (s >= 0 && s < S) ? s : 0;
+      int s = c < PIECES ? row(key) : 0;
+      s = (s >= 0 && s < nrows) ? s : 0;
       off[i] = ((uint32_t)s * Hkv + j) * (D * 2) + col * 16;
     }
     if (tid < kAttnKT) spos = pos(tid);

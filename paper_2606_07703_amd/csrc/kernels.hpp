@@ -19,19 +19,36 @@ struct Prob {
   size_t idx_group_stride() const { return ha ? (size_t)R * k : 0; }
 };
 
+// K/V storage of the sparse attention kernels: contiguous rows (table ==
+// nullptr) or a paged cache where token s lives in row
+// table[s / page_size] * page_size + s % page_size of num_pages * page_size.
+struct KvPages {
+  const int32_t *table = nullptr;
+  int page_size = 0;
+  int num_pages = 0;
+  __device__ __forceinline__ int row(int s) const {
+    if (!table) return s;
+    const int pg = table[s / page_size];
+    return (pg >= 0 && pg < num_pages) ? pg * page_size + s % page_size : -1;
+  }
+};
+
 // Dense (idx == nullptr) or sparse (idx != nullptr) attention, one wave per
 // (query, head chunk). o and/or lse may be null.
 hipError_t launch_attn_rowwise(const Prob &p, const void *q, const void *k, const void *v,
-                               const int32_t *idx, void *o, float *lse, hipStream_t st);
+                               const int32_t *idx, void *o, float *lse, hipStream_t st,
+                               KvPages pages = KvPages());
 
 // bf16 MFMA sparse attention for selection blocks of b >= 16 queries: each
 // gathered K/V row is shared by the b*G query rows of a KV head.
 bool sparse_query_mfma_supported(const Prob &p);
 hipError_t launch_sparse_query_mfma(const Prob &p, const void *q, const void *k, const void *v,
-                                    const int32_t *idx, void *o, hipStream_t st);
+                                    const int32_t *idx, void *o, hipStream_t st,
+                                    KvPages pages = KvPages());
 bool sparse_block_mfma_supported(const Prob &p);
 hipError_t launch_sparse_block_mfma(const Prob &p, const void *q, const void *k, const void *v,
-                                    const int32_t *idx, void *o, hipStream_t st);
+                                    const int32_t *idx, void *o, hipStream_t st,
+                                    KvPages pages = KvPages());
 
 // bf16 MFMA causal flash attention; o and/or lse (o == nullptr: normalisers only).
 bool dense_mfma_supported(const Prob &p);

@@ -19,17 +19,19 @@ namespace {
 
 constexpr int kMaxSupport = 4096;   // support row cached in LDS
 
-template <int D, int NW>
+template <int D, int NW, bool PAGED>
 __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
     int S, int Hq, int Hkv, int G, int b, int kk, size_t gstride, float scale_log2,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const int32_t *__restrict__ idx,
-    uint16_t *__restrict__ o) {
+    uint16_t *__restrict__ o, KvPages pages) {
   using L = AttnLayout<D>;
   constexpr int NT = NW * 64;
   __shared__ __align__(16) char lds[2][L::BUF];
   __shared__ int red_last[NW];
   __shared__ int ir[kMaxSupport];
+  // paged cache: the K/V row of each support entry (ir keeps the position)
+  __shared__ int irp[PAGED ? kMaxSupport : 1];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, c16 = lane & 15;
@@ -43,7 +45,12 @@ __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
   // block can use (any order).
   int last = -1;
   for (int c = tid; c < kk; c += NT) {
-    const int s = idx[(size_t)j * gstride + (size_t)r * kk + c];
+    int s = idx[(size_t)j * gstride + (size_t)r * kk + c];
+    if constexpr (PAGED) {
+      const int row = (s >= 0 && s < S) ? pages.row(s) : -1;
+      if (row < 0) s = -1;   // sentinel, or a page outside the cache: skipped
+      irp[c] = row;
+    }
     ir[c] = s;
     if (s >= 0 && s <= t1) last = c;
   }
@@ -67,8 +74,12 @@ __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
   auto pos_of = [&](int c0) {
     return [=](int e) { return c0 + e < kk ? ir[c0 + e] : -1; };
   };
+  auto row_of = [&](int c0) {
+    return [=](int e) { return c0 + e < kk ? (PAGED ? irp[c0 + e] : ir[c0 + e]) : -1; };
+  };
+  const int kv_rows = PAGED ? pages.num_pages * pages.page_size : S;
   if (ntiles > 0) {
-    stage.load(k, v, S, Hkv, j, tid, pos_of(0));
+    stage.load_rows(k, v, kv_rows, Hkv, j, tid, pos_of(0), row_of(0));
     stage.store(lds[0], tid);
   }
   drain_memory();
@@ -77,7 +88,9 @@ __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
   const int wave_tmin = t0 + row0 / G;
   for (int it = 0; it < ntiles; ++it) {
     const bool more = it + 1 < ntiles;
-    if (more) stage.load(k, v, S, Hkv, j, tid, pos_of((it + 1) * kAttnKT));
+    if (more)
+      stage.load_rows(k, v, kv_rows, Hkv, j, tid, pos_of((it + 1) * kAttnKT),
+                      row_of((it + 1) * kAttnKT));
     if (live) attn_tile<D, true, true>(lds[it & 1], bq, qt, scale_log2, wave_tmin, st, g, c16);
     if (more) stage.store(lds[(it + 1) & 1], tid);
     __syncthreads();
@@ -85,9 +98,9 @@ __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
   if (live) attn_finish<D>(st, qt, qh, qvalid, Hq, o, nullptr, g);
 }
 
-template <int D>
+template <int D, bool PAGED>
 hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
-                    const int32_t *idx, void *o, hipStream_t st) {
+                    const int32_t *idx, void *o, hipStream_t st, KvPages pages) {
   const int rows = p.b * p.G;
   int nw = (rows + kAttnQPW - 1) / kAttnQPW;
   nw = nw <= 1 ? 1 : nw <= 2 ? 2 : nw <= 4 ? 4 : 8;
@@ -95,10 +108,10 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
   dim3 grid(p.R, p.Hkv, chunks);
   const float sl2 = p.scale * kLog2e;
 #define SP_SB(NW)                                                                            \
-  hipLaunchKernelGGL((sparse_block_kernel<D, NW>), grid, dim3(NW * 64), 0, st, p.S, p.Hq,    \
-                     p.Hkv, p.G, p.b, p.k, p.idx_group_stride(), sl2, (const uint16_t *)q,      \
-                     (const uint16_t *)k,                                                     \
-                     (const uint16_t *)v, idx, (uint16_t *)o)
+  hipLaunchKernelGGL((sparse_block_kernel<D, NW, PAGED>), grid, dim3(NW * 64), 0, st, p.S,  \
+                     p.Hq, p.Hkv, p.G, p.b, p.k, p.idx_group_stride(), sl2,                   \
+                     (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, idx,      \
+                     (uint16_t *)o, pages)
   switch (nw) {
     case 1: SP_SB(1); break;
     case 2: SP_SB(2); break;
@@ -117,9 +130,13 @@ bool sparse_block_mfma_supported(const Prob &p) {
 }
 
 hipError_t launch_sparse_block_mfma(const Prob &p, const void *q, const void *k, const void *v,
-                                    const int32_t *idx, void *o, hipStream_t st) {
-  if (p.d == 64) return launch_d<64>(p, q, k, v, idx, o, st);
-  return launch_d<128>(p, q, k, v, idx, o, st);
+                                    const int32_t *idx, void *o, hipStream_t st, KvPages pages) {
+  if (pages.table) {
+    if (p.d == 64) return launch_d<64, true>(p, q, k, v, idx, o, st, pages);
+    return launch_d<128, true>(p, q, k, v, idx, o, st, pages);
+  }
+  if (p.d == 64) return launch_d<64, false>(p, q, k, v, idx, o, st, pages);
+  return launch_d<128, false>(p, q, k, v, idx, o, st, pages);
 }
 
 }  // namespace sp

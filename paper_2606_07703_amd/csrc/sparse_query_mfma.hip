@@ -59,7 +59,7 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
     int S, int Hq, int Hkv, int G, int b, int kk, size_t gstride, int n_groups, float scale_log2,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const int32_t *__restrict__ idx,
-    uint16_t *__restrict__ o) {
+    uint16_t *__restrict__ o, KvPages pages) {
   constexpr int KS = D / 32, DT = D / 16;
   constexpr int PPR = D / 8;         // 16-byte pieces per K/V row
   constexpr int VSTEP = 16 / PPR;    // row stride of a lane's V pieces
@@ -98,13 +98,14 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
 
   for (int c0 = 0; c0 < kk; c0 += kPosChunk) {
     const int n = min(kPosChunk, kk - c0);
-    // Copy the chunk of the support row into the wave's slot; entries that
-    // cannot contribute (sentinel, out of range, after t) become -1. The
-    // tile loop ends after the last usable entry.
+    // Copy the chunk of the support row into the wave's slot as K/V rows;
+    // entries that cannot contribute (sentinel, out of range, after t, a
+    // page outside the cache) become -1. The tile loop ends after the last
+    // usable entry.
     int last = -1;
     for (int e = lane; e < kPosChunk; e += 64) {
       int s = e < n ? row[c0 + e] : -1;
-      s = (s >= 0 && s <= t) ? s : -1;
+      s = (s >= 0 && s <= t) ? pages.row(s) : -1;
       ipos[e] = s;
       if (s >= 0) last = e;
     }
@@ -223,14 +224,14 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
 
 template <int D>
 hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
-                    const int32_t *idx, void *o, hipStream_t st) {
+                    const int32_t *idx, void *o, hipStream_t st, KvPages pages) {
   constexpr int NW = 4;
   const int n_groups = (p.S + NW - 1) / NW;
   hipLaunchKernelGGL((sparse_query_kernel<D, NW>), dim3(n_groups * p.Hkv), dim3(NW * 64), 0, st,
                      p.S, p.Hq, p.Hkv, p.G, p.b, p.k, p.idx_group_stride(), n_groups,
                      p.scale * kLog2e,
                      (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, idx,
-                     (uint16_t *)o);
+                     (uint16_t *)o, pages);
   return hipGetLastError();
 }
 
@@ -241,9 +242,9 @@ bool sparse_query_mfma_supported(const Prob &p) {
 }
 
 hipError_t launch_sparse_query_mfma(const Prob &p, const void *q, const void *k, const void *v,
-                                    const int32_t *idx, void *o, hipStream_t st) {
-  if (p.d == 64) return launch_d<64>(p, q, k, v, idx, o, st);
-  return launch_d<128>(p, q, k, v, idx, o, st);
+                                    const int32_t *idx, void *o, hipStream_t st, KvPages pages) {
+  if (p.d == 64) return launch_d<64>(p, q, k, v, idx, o, st, pages);
+  return launch_d<128>(p, q, k, v, idx, o, st, pages);
 }
 
 }  // namespace sp

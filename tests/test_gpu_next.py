@@ -276,3 +276,55 @@ def test_indexer_rejects_per_group_supports():
     x = torch.zeros(64, 64, dtype=torch.bfloat16, device="cuda")
     with pytest.raises(B.SparsePrefillError):
         B.sp_indexer_scores(p, x, x, torch.empty(64, 64, device="cuda"))
+
+
+# ------------------------------------------------------- paged K/V cache (f3)
+def _paged(k, v, ps, seed, extra=3):
+    """Scatter contiguous K/V over a larger cache of pages through a random table."""
+    S = k.shape[0]
+    npg = (S + ps - 1) // ps
+    perm = np.random.default_rng(seed).permutation(npg + extra)[:npg].astype(np.int32)
+    kp = torch.zeros((npg + extra, ps) + tuple(k.shape[1:]), dtype=k.dtype)
+    vp = torch.zeros_like(kp)
+    for lp in range(npg):
+        n = min(ps, S - lp * ps)
+        kp[perm[lp], :n] = k[lp * ps: lp * ps + n]
+        vp[perm[lp], :n] = v[lp * ps: lp * ps + n]
+    return kp, vp, torch.from_numpy(perm)
+
+
+@pytest.mark.parametrize("S,Hq,Hkv,d,b,dtype,ps,head_axis", [
+    (300, 8, 2, 128, 64, "bf16", 16, 0),
+    (300, 8, 2, 64, 16, "bf16", 7, 1),
+    (257, 8, 4, 128, 1, "bf16", 32, 0),
+    (200, 6, 3, 64, 4, "bf16", 1, 1),
+    (150, 4, 2, 64, 8, "f32", 10, 0),
+])
+def test_paged_sparse_attention(S, Hq, Hkv, d, b, dtype, ps, head_axis):
+    say(f"paged sparse S={S} d={d} b={b} {dtype} page={ps} head_axis={head_axis}")
+    k_ = 40
+    inp = make_inputs(S, Hq, Hkv, d, dtype=dtype, seed=S + ps, peaked=True)
+    if head_axis:
+        table = torch.stack([make_support(S, b, k_, seed=30 + j) for j in range(Hkv)])
+    else:
+        table = make_support(S, b, k_, seed=30, shuffle=True)
+    kp, vp, pt = _paged(inp.k, inp.v, ps, seed=S)
+    p = B.Problem(S, Hq, Hkv, d, topk=k_, block_q=b, dtype=dtype, head_axis=head_axis)
+    o = torch.empty(S, Hq, d, dtype=inp.q.dtype, device="cuda")
+    B.sp_sparse_gqa_attn_paged(p, inp.q.cuda(), kp.cuda(), vp.cuda(), pt.cuda(), table.cuda(), o)
+    # a logical page outside the cache drops its positions
+    bad = pt.clone()
+    bad[1] = kp.shape[0] + 5
+    o_bad = torch.empty_like(o)
+    B.sp_sparse_gqa_attn_paged(p, inp.q.cuda(), kp.cuda(), vp.cuda(), bad.cuda(), table.cuda(),
+                               o_bad)
+    torch.cuda.synchronize()
+    ref = oracle.sparse_paged(inp.q, kp, vp, pt, table, b)
+    assert max_err(o.cpu().double().numpy(), ref) <= tol_for(dtype)
+    ref_bad = oracle.sparse_paged(inp.q, kp, vp, bad, table, b)
+    assert max_err(o_bad.cpu().double().numpy(), ref_bad) <= tol_for(dtype)
+    # the paged result is the contiguous one
+    o_c = torch.empty_like(o)
+    B.sp_sparse_gqa_attn(p, inp.q.cuda(), inp.k.cuda(), inp.v.cuda(), table.cuda(), o_c)
+    torch.cuda.synchronize()
+    assert torch.equal(o, o_c)

@@ -226,3 +226,37 @@ def test_per_group_sparse_tables():
     ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, is_causal=True)
     assert np.allclose(oracle.sparse(q, k, v, full, b), ref.transpose(0, 1).numpy(),
                        rtol=1e-10, atol=1e-12)
+
+
+# ------------------------------------------------------------ paged K/V cache
+def test_paged_cache_matches_contiguous():
+    S, Hq, Hkv, d, b, kk, ps = 37, 4, 2, 8, 4, 11, 5
+    q, k, v = _qkv(S, Hq, Hkv, d, seed=20)
+    rng = np.random.default_rng(21)
+    R = (S + b - 1) // b
+    idx = np.full((R, kk), -1, dtype=np.int32)
+    for r in range(R):
+        t1 = min(r * b + b, S) - 1
+        m = min(kk, t1 + 1)
+        idx[r, :m] = rng.choice(t1 + 1, size=m, replace=False)
+    ref = oracle.sparse(q, k, v, idx, b)
+    # one page holding everything, identity table
+    one = oracle.sparse_paged(q, k[None], v[None], [0], idx, b)
+    assert np.array_equal(one, ref)
+    # pages scattered over a larger cache through a permuted table
+    npg = (S + ps - 1) // ps
+    perm = rng.permutation(npg + 3)[:npg]
+    kp = np.zeros((npg + 3, ps, Hkv, d))
+    vp = np.zeros((npg + 3, ps, Hkv, d))
+    for lp in range(npg):
+        n = min(ps, S - lp * ps)
+        kp[perm[lp], :n] = k[lp * ps: lp * ps + n]
+        vp[perm[lp], :n] = v[lp * ps: lp * ps + n]
+    assert np.array_equal(oracle.sparse_paged(q, kp, vp, perm, idx, b), ref)
+    # a logical page mapped outside the cache: its positions drop out of every support
+    bad = perm.copy()
+    bad[2] = npg + 3
+    dropped = idx.copy()
+    dropped[(dropped >= 2 * ps) & (dropped < 3 * ps)] = -1
+    assert np.array_equal(oracle.sparse_paged(q, kp, vp, bad, idx, b),
+                          oracle.sparse(q, k, v, dropped, b))
