@@ -110,6 +110,16 @@ typedef struct sp_problem {
                               query heads of the group (mass and tables
                               [Hkv, R, ...]). The indexer is head-collapsed and
                               takes 0 only. */
+  int32_t q_offset;     /* chunked prefill: the call covers query positions
+                           q_offset .. S-1 of a sequence whose keys are 0 .. S-1
+                           (S = seq_len). q, o, lse and q_idx then hold the
+                           S - q_offset chunk rows; k, v and k_idx all S rows;
+                           selection blocks are counted from q_offset (which
+                           must be a multiple of block_q), so R = ceil((S -
+                           q_offset) / b) and row r holds positions
+                           q_offset + r*b ... Used by sp_dense_attn,
+                           sp_indexer_scores, sp_topk_select and the sparse
+                           attention calls; 0 elsewhere. */
 } sp_problem;
 
 /*

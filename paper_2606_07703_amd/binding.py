@@ -32,7 +32,7 @@ class SpProblem(ctypes.Structure):
         "seq_len", "num_q_heads", "num_kv_heads", "head_dim", "index_dim", "topk", "block_q",
         "causal", "local_window", "agg", "relu", "dtype")] + [
         ("attn_scale", ctypes.c_float), ("index_scale", ctypes.c_float),
-        ("head_axis", ctypes.c_int32)]
+        ("head_axis", ctypes.c_int32), ("q_offset", ctypes.c_int32)]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -53,10 +53,15 @@ class Problem:
     attn_scale: float = 0.0
     index_scale: float = 0.0
     head_axis: int = 0    # 1: one support per KV group (tables gain a leading Hkv axis)
+    q_offset: int = 0     # chunked prefill: this call covers query positions q_offset..S-1
+
+    @property
+    def num_queries(self) -> int:
+        return self.seq_len - self.q_offset
 
     @property
     def num_blocks(self) -> int:
-        return (self.seq_len + self.block_q - 1) // self.block_q
+        return (self.num_queries + self.block_q - 1) // self.block_q
 
     @property
     def table_rows(self) -> tuple:
@@ -69,7 +74,7 @@ class Problem:
                          self.index_dim, self.topk, self.block_q, self.causal,
                          self.local_window, SP_AGG[self.agg], int(bool(self.relu)),
                          SP_DTYPE[self.dtype], self.attn_scale, self.index_scale,
-                         int(self.head_axis))
+                         int(self.head_axis), int(self.q_offset))
 
 
 class SparsePrefillError(RuntimeError):
@@ -155,9 +160,10 @@ def sp_dense_attn(p: Problem, q, k, v, o=None, lse=None, stream=None) -> None:
     S, Hq, Hkv, d = p.seq_len, p.num_q_heads, p.num_kv_heads, p.head_dim
     dt = TORCH_DTYPE[p.dtype]
     c = p.to_c()
-    _call("sp_dense_attn", ctypes.byref(c), _ptr(q, "q", (S, Hq, d), dt),
+    nq = p.num_queries
+    _call("sp_dense_attn", ctypes.byref(c), _ptr(q, "q", (nq, Hq, d), dt),
           _ptr(k, "k", (S, Hkv, d), dt), _ptr(v, "v", (S, Hkv, d), dt),
-          _ptr(o, "o", (S, Hq, d), dt), _ptr(lse, "lse", (S, Hq), torch.float32),
+          _ptr(o, "o", (nq, Hq, d), dt), _ptr(lse, "lse", (nq, Hq), torch.float32),
           _stream(stream))
 
 
@@ -174,7 +180,8 @@ def sp_indexer_scores(p: Problem, q_idx, k_idx, scores, stream=None) -> None:
     S, di = p.seq_len, p.index_dim
     dt = TORCH_DTYPE[p.dtype]
     c = p.to_c()
-    _call("sp_indexer_scores", ctypes.byref(c), _ptr(q_idx, "q_idx", (S, di), dt),
+    _call("sp_indexer_scores", ctypes.byref(c),
+          _ptr(q_idx, "q_idx", (p.num_queries, di), dt),
           _ptr(k_idx, "k_idx", (S, di), dt),
           _ptr(scores, "scores", (p.num_blocks, S), torch.float32), _stream(stream))
 
@@ -197,10 +204,10 @@ def sp_sparse_gqa_attn(p: Problem, q, k, v, idx, o, stream=None) -> None:
     S, Hq, Hkv, d = p.seq_len, p.num_q_heads, p.num_kv_heads, p.head_dim
     dt = TORCH_DTYPE[p.dtype]
     c = p.to_c()
-    _call("sp_sparse_gqa_attn", ctypes.byref(c), _ptr(q, "q", (S, Hq, d), dt),
+    _call("sp_sparse_gqa_attn", ctypes.byref(c), _ptr(q, "q", (p.num_queries, Hq, d), dt),
           _ptr(k, "k", (S, Hkv, d), dt), _ptr(v, "v", (S, Hkv, d), dt),
           _ptr(idx, "idx", p.table_rows + (p.topk,), torch.int32),
-          _ptr(o, "o", (S, Hq, d), dt), _stream(stream))
+          _ptr(o, "o", (p.num_queries, Hq, d), dt), _stream(stream))
 
 
 def sp_indexer_topk(p: Problem, q_idx, k_idx, idx, workspace=None, stream=None) -> None:
@@ -254,12 +261,13 @@ def sp_sparse_gqa_attn_paged(p: Problem, q, k_pages, v_pages, page_table, idx, o
     dt = TORCH_DTYPE[p.dtype]
     npg, ps = (k_pages.shape[0], k_pages.shape[1]) if k_pages is not None else (0, 0)
     c = p.to_c()
-    _call("sp_sparse_gqa_attn_paged", ctypes.byref(c), _ptr(q, "q", (S, Hq, d), dt),
+    _call("sp_sparse_gqa_attn_paged", ctypes.byref(c),
+          _ptr(q, "q", (p.num_queries, Hq, d), dt),
           _ptr(k_pages, "k_pages", (npg, ps, Hkv, d), dt),
           _ptr(v_pages, "v_pages", (npg, ps, Hkv, d), dt),
           _ptr(page_table, "page_table", ((S + ps - 1) // max(ps, 1),), torch.int32), ps, npg,
           _ptr(idx, "idx", p.table_rows + (p.topk,), torch.int32),
-          _ptr(o, "o", (S, Hq, d), dt), _stream(stream))
+          _ptr(o, "o", (p.num_queries, Hq, d), dt), _stream(stream))
 
 
 def sp_workspace_bytes(p: Problem, op: str) -> int:

@@ -24,6 +24,7 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 int check_common(const sp_problem *p) {
   if (!p) return SP_ERR_NULL;
   if (p->seq_len < 1 || p->num_q_heads < 1 || p->num_kv_heads < 1) return SP_ERR_SHAPE;
+  if (p->q_offset < 0 || p->q_offset >= p->seq_len) return SP_ERR_SHAPE;
   if (p->num_q_heads % p->num_kv_heads != 0) return SP_ERR_SHAPE;
   if (p->causal != 1) return SP_ERR_UNSUPPORTED;
   if (p->dtype != SP_DTYPE_F32 && p->dtype != SP_DTYPE_BF16) return SP_ERR_UNSUPPORTED;
@@ -45,6 +46,8 @@ int check_heads(const sp_problem *p) {
 int check_selection(const sp_problem *p) {
   if (p->block_q < 1) return SP_ERR_SHAPE;
   if (p->head_axis != 0 && p->head_axis != 1) return SP_ERR_SHAPE;
+  // a chunk starts on a selection-block boundary
+  if (p->q_offset % p->block_q != 0) return SP_ERR_SHAPE;
   if (p->topk < 1) return SP_ERR_SHAPE;
   if (p->local_window < 0 || p->local_window > p->topk) return SP_ERR_SHAPE;
   return SP_OK;
@@ -65,7 +68,9 @@ Prob resolve(const sp_problem *p) {
   r.di = p->index_dim;
   r.k = p->topk;
   r.b = p->block_q < 1 ? 1 : p->block_q;
-  r.R = (r.S + r.b - 1) / r.b;
+  r.qo = p->q_offset;
+  r.nq = r.S - r.qo;
+  r.R = (r.nq + r.b - 1) / r.b;
   r.W = p->local_window;
   r.agg = p->agg;
   r.relu = p->relu;
@@ -121,7 +126,8 @@ int sp_dense_attn(const sp_problem *p, const void *q, const void *k, const void 
     return SP_ERR_ALIGN;
   SP_TRY(check_device());
   const Prob r = resolve(p);
-  if (dense_mfma_supported(r)) return launched(launch_dense_mfma(r, q, k, v, o, lse, stream));
+  if (r.qo == 0 && dense_mfma_supported(r))
+    return launched(launch_dense_mfma(r, q, k, v, o, lse, stream));
   return launched(launch_attn_rowwise(r, q, k, v, nullptr, o, lse, stream));
 }
 
@@ -131,6 +137,7 @@ int sp_oracle_support(const sp_problem *p, const void *q, const void *k, const f
   SP_TRY(check_heads(p));
   SP_TRY(check_selection(p));
   SP_TRY(check_agg(p));
+  if (p->q_offset != 0) return SP_ERR_UNSUPPORTED;   // the oracle runs on whole sequences
   if (!q || !k || !lse || !mass) return SP_ERR_NULL;
   if (!aligned16(q) || !aligned16(k) || !aligned16(lse) || !aligned16(mass)) return SP_ERR_ALIGN;
   SP_TRY(check_device());
@@ -198,6 +205,7 @@ int sp_indexer_topk(const sp_problem *p, const void *q_idx, const void *k_idx, i
     return SP_ERR_UNSUPPORTED;
   if (p->relu != 0 && p->relu != 1) return SP_ERR_SHAPE;
   if (p->block_q != 1) return SP_ERR_UNSUPPORTED;   // the block form aggregates in-kernel
+  if (p->q_offset != 0) return SP_ERR_UNSUPPORTED;
   if (!q_idx || !k_idx || !idx) return SP_ERR_NULL;
   if (!aligned16(q_idx) || !aligned16(k_idx) || !aligned16(idx) || !aligned16(workspace))
     return SP_ERR_ALIGN;

@@ -28,9 +28,10 @@ template <typename T, int D, int HPW, bool SPARSE>
 __global__ __launch_bounds__(64) void attn_rowwise_kernel(
     int S, int Hq, int Hkv, int G, float scale_log2, const T *__restrict__ q,
     const T *__restrict__ k, const T *__restrict__ v, const int32_t *__restrict__ idx, int kk,
-    int b, size_t gstride, T *__restrict__ o, float *__restrict__ lse, KvPages pages) {
+    int b, size_t gstride, T *__restrict__ o, float *__restrict__ lse, KvPages pages, int qo) {
+  // q, o and lse are addressed by position: the host shifts them back by qo rows
   constexpr int EPL = D / 16;
-  const int t = blockIdx.x;
+  const int t = qo + blockIdx.x;
   const int h0 = blockIdx.y * HPW;
   const int j = h0 / G;
   const int lane = threadIdx.x;
@@ -54,7 +55,7 @@ __global__ __launch_bounds__(64) void attn_rowwise_kernel(
   }
 
   const int n = SPARSE ? kk : t + 1;
-  const int32_t *ir = SPARSE ? idx + (size_t)j * gstride + (size_t)(t / b) * kk : nullptr;
+  const int32_t *ir = SPARSE ? idx + (size_t)j * gstride + (size_t)((t - qo) / b) * kk : nullptr;
   for (int base = 0; base < n; base += 4) {
     const int i = base + grp;
     int s = i;
@@ -131,16 +132,21 @@ __global__ __launch_bounds__(64) void attn_rowwise_kernel(
 template <typename T, int D, int HPW>
 hipError_t launch_t(const Prob &p, const void *q, const void *k, const void *v,
                     const int32_t *idx, void *o, float *lse, hipStream_t st, KvPages pages) {
-  dim3 grid(p.S, p.Hq / HPW);
+  dim3 grid(p.nq, p.Hq / HPW);
   const float sl2 = p.scale * kLog2e;
+  // chunk rows are addressed by position
+  const size_t shift = (size_t)p.qo * p.Hq;
+  const T *qs = (const T *)q - shift * D;
+  T *os = o ? (T *)o - shift * D : nullptr;
+  float *ls = lse ? lse - shift : nullptr;
   if (idx)
     hipLaunchKernelGGL((attn_rowwise_kernel<T, D, HPW, true>), grid, dim3(64), 0, st, p.S,
-                       p.Hq, p.Hkv, p.G, sl2, (const T *)q, (const T *)k, (const T *)v, idx,
-                       p.k, p.b, p.idx_group_stride(), (T *)o, lse, pages);
+                       p.Hq, p.Hkv, p.G, sl2, qs, (const T *)k, (const T *)v, idx, p.k, p.b,
+                       p.idx_group_stride(), os, ls, pages, p.qo);
   else
     hipLaunchKernelGGL((attn_rowwise_kernel<T, D, HPW, false>), grid, dim3(64), 0, st, p.S,
-                       p.Hq, p.Hkv, p.G, sl2, (const T *)q, (const T *)k, (const T *)v,
-                       nullptr, 0, 1, (size_t)0, (T *)o, lse, KvPages());
+                       p.Hq, p.Hkv, p.G, sl2, qs, (const T *)k, (const T *)v, nullptr, 0, 1,
+                       (size_t)0, os, ls, KvPages(), p.qo);
   return hipGetLastError();
 }
 

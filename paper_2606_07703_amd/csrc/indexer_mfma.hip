@@ -110,27 +110,32 @@ __device__ __forceinline__ float reduce_scatter(const float (&v)[2], Op op) {
 // workgroup i (which the hardware places on XCD i % 8) takes item
 // xcd_range_start + i / 8: each XCD walks a contiguous run of items and its L2
 // sees each key chunk once for several query groups.
+// g0: first query group (a chunk starting at g0 * QG covers groups g0 ..).
 template <int QG, int KC>
-__device__ __forceinline__ void decode_item(int i, int n_items, int S, int &qg, int &kc) {
+__device__ __forceinline__ void decode_item(int i, int n_items, int S, int g0, int &qg,
+                                            int &kc) {
   const int x = i % kXcds, j = i / kXcds;
   const int lin = x * (n_items / kXcds) + min(x, n_items % kXcds) + j;
   const int nqg = (S + QG - 1) / QG;
   int c = 0, base = 0;
   for (;;) {
-    const int cnt = nqg - c * KC / QG;
-    if (lin < base + cnt) break;
+    const int first = max(g0, c * KC / QG);
+    const int cnt = nqg - first;
+    if (lin < base + cnt) {
+      qg = first + (lin - base);
+      break;
+    }
     base += cnt;
     ++c;
   }
   kc = c;
-  qg = c * KC / QG + (lin - base);
 }
 
 template <int QG, int KC>
-int count_items(int S) {
+int count_items(int S, int g0) {
   const int nqg = (S + QG - 1) / QG, nkc = (S + KC - 1) / KC;
   int n = 0;
-  for (int c = 0; c < nkc; ++c) n += nqg - c * KC / QG;
+  for (int c = 0; c < nkc; ++c) n += nqg - max(g0, c * KC / QG);
   return n;
 }
 
@@ -175,8 +180,8 @@ struct KeyStageT {
 };
 
 template <int DI, int BQ, bool MAXPOS, int NW, int KC>
-__global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_items, int agg,
-                                                                int relu, float scale,
+__global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_items, int g0,
+                                                                int agg, int relu, float scale,
                                                                 const uint16_t *__restrict__ qi,
                                                                 const uint16_t *__restrict__ ki,
                                                                 float *__restrict__ Y) {
@@ -192,7 +197,7 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_ite
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, c16 = lane & 15;
   int qg, kc;
-  decode_item<QG, KC>(blockIdx.x, n_items, S, qg, kc);
+  decode_item<QG, KC>(blockIdx.x, n_items, S, g0, qg, kc);
   const int q0 = qg * QG;
   const int k_begin = kc * KC;
   const int q_last = min(q0 + QG, S) - 1;
@@ -341,7 +346,7 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_ite
 }
 
 template <int DI, bool VEC>
-__global__ __launch_bounds__(256) void indexer_rows_kernel(int S, int relu, float scale,
+__global__ __launch_bounds__(256) void indexer_rows_kernel(int S, int qo, int relu, float scale,
                                                            const uint16_t *__restrict__ qi,
                                                            const uint16_t *__restrict__ ki,
                                                            float *__restrict__ Z) {
@@ -352,7 +357,7 @@ __global__ __launch_bounds__(256) void indexer_rows_kernel(int S, int relu, floa
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, c16 = lane & 15;
-  const int q0 = blockIdx.x * QG;
+  const int q0 = qo + blockIdx.x * QG;   // qi and Z are addressed by position
   const int k_begin = blockIdx.y * kKC;
   const int q_last = min(q0 + QG, S) - 1;
   if (k_begin > q_last) return;
@@ -428,29 +433,35 @@ __global__ __launch_bounds__(256) void indexer_rows_kernel(int S, int relu, floa
 template <int DI>
 hipError_t launch_di(const Prob &p, const void *qi, const void *ki, float *scores,
                      hipStream_t st) {
-  const uint16_t *q = (const uint16_t *)qi, *k = (const uint16_t *)ki;
+  // chunk rows (a call starting at position qo) are addressed by position:
+  // q_idx and per-query scores are shifted back by qo rows, block scores by
+  // qo / b rows
+  const uint16_t *q = (const uint16_t *)qi - (size_t)p.qo * DI, *k = (const uint16_t *)ki;
   if (p.b == 1) {
-    dim3 grid((p.S + 255) / 256, (p.S + kKC - 1) / kKC);
+    float *z = scores - (size_t)p.qo * p.S;
+    dim3 grid((p.nq + 255) / 256, (p.S + kKC - 1) / kKC);
     if (p.S % 4 == 0)
-      hipLaunchKernelGGL((indexer_rows_kernel<DI, true>), grid, dim3(256), 0, st, p.S, p.relu,
-                         p.iscale, q, k, scores);
+      hipLaunchKernelGGL((indexer_rows_kernel<DI, true>), grid, dim3(256), 0, st, p.S, p.qo,
+                         p.relu, p.iscale, q, k, z);
     else
-      hipLaunchKernelGGL((indexer_rows_kernel<DI, false>), grid, dim3(256), 0, st, p.S, p.relu,
-                         p.iscale, q, k, scores);
+      hipLaunchKernelGGL((indexer_rows_kernel<DI, false>), grid, dim3(256), 0, st, p.S, p.qo,
+                         p.relu, p.iscale, q, k, z);
     return hipGetLastError();
   }
   constexpr int NW = 8, KC = 1024;
-  const int n_items = count_items<NW * kQW, KC>(p.S);
+  const int g0 = p.qo / (NW * kQW);   // a multiple of the query group (checked)
+  float *y = scores - (size_t)(p.qo / p.b) * p.S;
+  const int n_items = count_items<NW * kQW, KC>(p.S, g0);
   const bool maxpos = p.agg == SP_AGG_MAX && p.iscale >= 0.f;
 #define SP_BLK(BQ)                                                                           \
   if (maxpos)                                                                                \
     hipLaunchKernelGGL((indexer_block_kernel<DI, BQ, true, NW, KC>), dim3(n_items),          \
-                       dim3(NW * 64), 0, st, p.S, n_items, p.agg, p.relu, p.iscale, q, k,    \
-                       scores);                                                              \
+                       dim3(NW * 64), 0, st, p.S, n_items, g0, p.agg, p.relu, p.iscale, q,   \
+                       k, y);                                                                \
   else                                                                                       \
     hipLaunchKernelGGL((indexer_block_kernel<DI, BQ, false, NW, KC>), dim3(n_items),         \
-                       dim3(NW * 64), 0, st, p.S, n_items, p.agg, p.relu, p.iscale, q, k,    \
-                       scores)
+                       dim3(NW * 64), 0, st, p.S, n_items, g0, p.agg, p.relu, p.iscale, q,   \
+                       k, y)
   switch (p.b) {
     case 16: SP_BLK(16); break;
     case 32: SP_BLK(32); break;
@@ -464,8 +475,10 @@ hipError_t launch_di(const Prob &p, const void *qi, const void *ki, float *score
 }  // namespace
 
 bool indexer_mfma_supported(const Prob &p) {
+  // a chunked call of the block kernel starts on one of its 512-query groups
   return p.dtype == SP_DTYPE_BF16 && (p.di == 64 || p.di == 128 || p.di == 256) &&
-         (p.b == 1 || p.b == 16 || p.b == 32 || p.b == 64 || p.b == 128);
+         (p.b == 1 ||
+          ((p.b == 16 || p.b == 32 || p.b == 64 || p.b == 128) && p.qo % 512 == 0));
 }
 
 hipError_t launch_indexer_mfma(const Prob &p, const void *qi, const void *ki, float *scores,

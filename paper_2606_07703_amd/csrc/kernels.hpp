@@ -13,6 +13,8 @@ namespace sp {
 struct Prob {
   int S, Hq, Hkv, G, d, di, k, b, R, W, agg, relu, dtype;
   int ha;        // head axis: 0 one support shared by all heads, 1 one per KV group
+  int qo;        // position of the first query row (a chunk [qo, S) of the sequence)
+  int nq;        // query rows, S - qo; R counts the chunk's selection blocks
   float scale;   // attention logit scale
   float iscale;  // indexer score scale
   // elements between the support tables of consecutive KV groups

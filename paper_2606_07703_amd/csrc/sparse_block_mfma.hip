@@ -24,7 +24,8 @@ __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
     int S, int Hq, int Hkv, int G, int b, int kk, size_t gstride, float scale_log2,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const int32_t *__restrict__ idx,
-    uint16_t *__restrict__ o, KvPages pages) {
+    uint16_t *__restrict__ o, KvPages pages, int qo) {
+  // q and o are addressed by position: the host shifts them back by qo rows
   using L = AttnLayout<D>;
   constexpr int NT = NW * 64;
   __shared__ __align__(16) char lds[2][L::BUF];
@@ -35,8 +36,8 @@ __global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, c16 = lane & 15;
-  const int r = blockIdx.x, j = blockIdx.y;
-  const int t0 = r * b;
+  const int r = blockIdx.x, j = blockIdx.y;   // r counts blocks from the chunk start
+  const int t0 = qo + r * b;
   const int t1 = min(t0 + b, S) - 1;
   const int nrows = (t1 - t0 + 1) * G;
   const int row0 = blockIdx.z * (NW * kAttnQPW) + wave * kAttnQPW;
@@ -107,11 +108,13 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
   const int chunks = (rows + nw * kAttnQPW - 1) / (nw * kAttnQPW);
   dim3 grid(p.R, p.Hkv, chunks);
   const float sl2 = p.scale * kLog2e;
+  const size_t shift = (size_t)p.qo * p.Hq * D;   // chunk rows addressed by position
+  const uint16_t *qs = (const uint16_t *)q - shift;
+  uint16_t *os = (uint16_t *)o - shift;
 #define SP_SB(NW)                                                                            \
   hipLaunchKernelGGL((sparse_block_kernel<D, NW, PAGED>), grid, dim3(NW * 64), 0, st, p.S,  \
                      p.Hq, p.Hkv, p.G, p.b, p.k, p.idx_group_stride(), sl2,                   \
-                     (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, idx,      \
-                     (uint16_t *)o, pages)
+                     qs, (const uint16_t *)k, (const uint16_t *)v, idx, os, pages, p.qo)
   switch (nw) {
     case 1: SP_SB(1); break;
     case 2: SP_SB(2); break;

@@ -59,7 +59,8 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
     int S, int Hq, int Hkv, int G, int b, int kk, size_t gstride, int n_groups, float scale_log2,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const int32_t *__restrict__ idx,
-    uint16_t *__restrict__ o, KvPages pages) {
+    uint16_t *__restrict__ o, KvPages pages, int qo) {
+  // q and o are addressed by position: the host shifts them back by qo rows
   constexpr int KS = D / 32, DT = D / 16;
   constexpr int PPR = D / 8;         // 16-byte pieces per K/V row
   constexpr int VSTEP = 16 / PPR;    // row stride of a lane's V pieces
@@ -73,9 +74,9 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
   const int vpiece = c16 % PPR, vsub = c16 / PPR;
   const int j = blockIdx.x % Hkv;
   const int grp = n_groups - 1 - blockIdx.x / Hkv;   // longest queries first
-  const int t = grp * NW + wave;
+  const int t = qo + grp * NW + wave;
   if (t >= S) return;   // no workgroup barrier below: waves are independent
-  const int32_t *row = idx + (size_t)j * gstride + (size_t)(t / b) * kk;
+  const int32_t *row = idx + (size_t)j * gstride + (size_t)((t - qo) / b) * kk;
   int *ipos = sh.pos[wave];
   char *vb = sh.vbuf[wave];
 
@@ -226,12 +227,13 @@ template <int D>
 hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
                     const int32_t *idx, void *o, hipStream_t st, KvPages pages) {
   constexpr int NW = 4;
-  const int n_groups = (p.S + NW - 1) / NW;
+  const int n_groups = (p.nq + NW - 1) / NW;
+  const size_t shift = (size_t)p.qo * p.Hq * D;   // chunk rows addressed by position
   hipLaunchKernelGGL((sparse_query_kernel<D, NW>), dim3(n_groups * p.Hkv), dim3(NW * 64), 0, st,
                      p.S, p.Hq, p.Hkv, p.G, p.b, p.k, p.idx_group_stride(), n_groups,
                      p.scale * kLog2e,
-                     (const uint16_t *)q, (const uint16_t *)k, (const uint16_t *)v, idx,
-                     (uint16_t *)o, pages);
+                     (const uint16_t *)q - shift, (const uint16_t *)k, (const uint16_t *)v, idx,
+                     (uint16_t *)o - shift, pages, p.qo);
   return hipGetLastError();
 }
 

@@ -76,11 +76,13 @@ __global__ __launch_bounds__(kCols) void mass_rowwise_kernel(
 
 template <typename T, int DI>
 __global__ __launch_bounds__(kCols) void indexer_rowwise_kernel(
-    int S, int b, int agg, int relu, float iscale, const T *__restrict__ qi,
+    int S, int qo, int b, int agg, int relu, float iscale, const T *__restrict__ qi,
     const T *__restrict__ ki, float *__restrict__ scores) {
+  // qi is addressed by position (shifted back by qo rows by the host); rows of
+  // scores count blocks from the chunk start qo
   __shared__ float qs[DI];
   const int r = blockIdx.x;
-  const int t0 = r * b;
+  const int t0 = qo + r * b;
   const int t1 = min(t0 + b, S) - 1;
   const int c0 = blockIdx.y * kCols;
   if (c0 > t1) return;
@@ -142,8 +144,9 @@ hipError_t launch_indexer_rowwise(const Prob &p, const void *qi, const void *ki,
                                   hipStream_t st) {
   const dim3 grid = grid_for(p);
 #define SP_IDX(T, DI)                                                                        \
-  hipLaunchKernelGGL((indexer_rowwise_kernel<T, DI>), grid, dim3(kCols), 0, st, p.S, p.b,   \
-                     p.agg, p.relu, p.iscale, (const T *)qi, (const T *)ki, scores)
+  hipLaunchKernelGGL((indexer_rowwise_kernel<T, DI>), grid, dim3(kCols), 0, st, p.S, p.qo,   \
+                     p.b, p.agg, p.relu, p.iscale, (const T *)qi - (size_t)p.qo * DI,        \
+                     (const T *)ki, scores)
   if (p.dtype == SP_DTYPE_BF16) {
     if (p.di == 64) SP_IDX(bf16, 64);
     else if (p.di == 128) SP_IDX(bf16, 128);

@@ -64,7 +64,7 @@ constexpr int kRun = 16;                      // consecutive positions per run
 constexpr int kRegSub = 4;                    // runs per thread
 constexpr int kRegCap = kRegNT * kRun * kRegSub;   // 32768 candidates
 
-__global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int b, int k, int W,
+__global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int qo, int b, int k, int W,
                                                           const float *__restrict__ scores,
                                                           int32_t *__restrict__ idx) {
   constexpr int NT = kRegNT;
@@ -74,7 +74,7 @@ __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int b, int k, i
 
   const int r = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63;
-  const int t1 = min(r * b + b, S) - 1;
+  const int t1 = min(qo + r * b + b, S) - 1;   // rows count blocks from the chunk start
   const int L = t1 + 1;
   // blockIdx.y: the KV group of a per-group table (0 for a shared one)
   const size_t row_id = (size_t)blockIdx.y * gridDim.x + r;
@@ -199,7 +199,7 @@ constexpr int kEmitPer = 16;
 constexpr int kEmitChunk = kNT * kEmitPer;
 constexpr int kEmitStride = kNT + 4;   // LDS column stride: conflict-free writes and reads
 
-__global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int b, int k, int W,
+__global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, int k, int W,
                                                         const float *__restrict__ scores,
                                                         int32_t *__restrict__ idx) {
   __shared__ uint32_t hist[2048];
@@ -209,7 +209,7 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int b, int k, int
 
   const int r = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63;
-  const int t1 = min(r * b + b, S) - 1;
+  const int t1 = min(qo + r * b + b, S) - 1;   // rows count blocks from the chunk start
   const int L = t1 + 1;
   // blockIdx.y: the KV group of a per-group table (0 for a shared one)
   const size_t row_id = (size_t)blockIdx.y * gridDim.x + r;
@@ -307,14 +307,14 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int b, int k, int
 
 hipError_t launch_topk(const Prob &p, const float *scores, int32_t *idx, hipStream_t st) {
   // Longest candidate range of any row: the last block's causal length minus the window.
-  const int Lmax = min(p.R * p.b, p.S);
+  const int Lmax = min(p.qo + p.R * p.b, p.S);
   const int ncmax = Lmax - min(p.W, p.k);
   if (ncmax <= kRegCap)
     hipLaunchKernelGGL(topk_reg_kernel, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kRegNT), 0, st, p.S,
-                       p.b, p.k, p.W, scores, idx);
+                       p.qo, p.b, p.k, p.W, scores, idx);
   else
     hipLaunchKernelGGL(topk_rows_kernel, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kNT), 0, st, p.S,
-                       p.b, p.k, p.W, scores, idx);
+                       p.qo, p.b, p.k, p.W, scores, idx);
   return hipGetLastError();
 }
 

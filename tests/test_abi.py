@@ -211,3 +211,21 @@ def test_kl_errors():
     assert f(ctypes.byref(pc), P(16), 2, P(16), P(18), None, None, None, None) == ALIGN
     if NO_DEVICE:
         assert f(ctypes.byref(pc), P(16), 2, P(16), P(16), P(16), P(16), P(16), None) == NODEV
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(q_offset=-1), SHAPE),
+    (dict(q_offset=128), SHAPE),           # no query rows left (S = 128)
+    (dict(q_offset=6, block_q=4), SHAPE),  # a chunk starts on a selection-block boundary
+    (dict(head_axis=2), SHAPE),
+])
+def test_chunk_and_head_axis_errors(kw, expect):
+    assert sparse(prob(**kw)) == expect
+    assert topk(prob(**kw)) == expect
+
+
+def test_oracle_support_and_fused_reject_chunks():
+    assert oracle_support(prob(q_offset=8)) == UNSUP
+    p = prob(q_offset=8, block_q=1)
+    n = ctypes.c_size_t()
+    assert lib().sp_indexer_topk(ctypes.byref(p), A, A2, A3, A4, 1 << 30, None) == UNSUP

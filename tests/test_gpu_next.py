@@ -328,3 +328,99 @@ def test_paged_sparse_attention(S, Hq, Hkv, d, b, dtype, ps, head_axis):
     B.sp_sparse_gqa_attn(p, inp.q.cuda(), inp.k.cuda(), inp.v.cuda(), table.cuda(), o_c)
     torch.cuda.synchronize()
     assert torch.equal(o, o_c)
+
+
+# ------------------------------------------------ chunked prefill rows (f3)
+from synth import make_scores  # noqa: E402
+
+
+@pytest.mark.parametrize("S,qo,b,d,dtype", [(300, 128, 64, 128, "bf16"), (300, 48, 16, 64, "bf16"),
+                                            (257, 77, 1, 128, "bf16"), (200, 40, 4, 64, "f32"),
+                                            (200, 199, 1, 64, "bf16")])
+def test_chunked_sparse_attention(S, qo, b, d, dtype):
+    say(f"chunked sparse S={S} q_offset={qo} b={b} d={d} {dtype}")
+    Hq, Hkv, k = 8, 2, 40
+    inp = make_inputs(S, Hq, Hkv, d, dtype=dtype, seed=S + qo, peaked=True)
+    full = make_support(S, b, k, seed=qo)            # tables of the whole sequence
+    table = full[qo // b:].contiguous()              # the chunk's blocks
+    p = B.Problem(S, Hq, Hkv, d, topk=k, block_q=b, dtype=dtype, q_offset=qo)
+    o = torch.empty(S - qo, Hq, d, dtype=inp.q.dtype, device="cuda")
+    B.sp_sparse_gqa_attn(p, inp.q[qo:].contiguous().cuda(), inp.k.cuda(), inp.v.cuda(),
+                         table.cuda(), o)
+    kp, vp, pt = _paged(inp.k, inp.v, 16, seed=S)
+    o2 = torch.empty_like(o)
+    B.sp_sparse_gqa_attn_paged(p, inp.q[qo:].contiguous().cuda(), kp.cuda(), vp.cuda(),
+                               pt.cuda(), table.cuda(), o2)
+    torch.cuda.synchronize()
+    ref = oracle.sparse(inp.q, inp.k, inp.v, full, b, rows=np.arange(qo, S))
+    assert max_err(o.cpu().double().numpy(), ref) <= tol_for(dtype)
+    assert torch.equal(o, o2)
+
+
+@pytest.mark.parametrize("S,qo,b,W", [(300, 100, 1, 0), (300, 96, 32, 5), (5000, 4096, 64, 0)])
+def test_chunked_topk(S, qo, b, W):
+    say(f"chunked topk S={S} q_offset={qo} b={b} W={W}")
+    k = 37
+    R = (S - qo + b - 1) // b
+    scores = make_scores(R, S, seed=S + qo, kind="relu")
+    p = B.Problem(S, 1, 1, 64, topk=k, block_q=b, local_window=W, dtype="f32", q_offset=qo)
+    idx = torch.empty(R, k, dtype=torch.int32, device="cuda")
+    B.sp_topk_select(p, scores.cuda(), idx)
+    torch.cuda.synchronize()
+    lens = np.array([min(qo + r * b + b, S) for r in range(R)])
+    ref = oracle.topk(scores.numpy().astype(np.float64), lens, k, W)
+    assert np.array_equal(idx.cpu().numpy(), ref)
+
+
+@pytest.mark.parametrize("S,qo,b,di", [(700, 100, 1, 128), (1200, 512, 64, 128),
+                                       (700, 128, 64, 64), (700, 64, 16, 256)])
+def test_chunked_indexer_scores(S, qo, b, di):
+    say(f"chunked indexer S={S} q_offset={qo} b={b} d_idx={di}")
+    inp = make_inputs(S, 1, 1, 64, index_dim=di, dtype="bf16", seed=S + b, needles=4)
+    p = B.Problem(S, 1, 1, 64, index_dim=di, topk=8, block_q=b, q_offset=qo)
+    R = p.num_blocks
+    sc = torch.full((R, S), float("nan"), device="cuda")
+    B.sp_indexer_scores(p, inp.q_idx[qo:].contiguous().cuda(), inp.k_idx.cuda(), sc)
+    torch.cuda.synchronize()
+    units = range(qo // b, qo // b + R)
+    ref = oracle.support_scores("indexer", units, b, q_idx=inp.q_idx, k_idx=inp.k_idx)
+    got = sc.cpu().double().numpy()
+    scale = np.abs(ref).max()
+    for r in range(R):
+        L = min(qo + r * b + b, S)
+        assert max_err(got[r, :L], ref[r, :L]) <= 2e-6 * scale
+        assert np.all(np.isnan(got[r, L:]))
+
+
+def test_chunked_dense_and_pipeline_equal_whole_sequence():
+    S, Hq, Hkv, d, di, k, b, qo = 640, 8, 2, 128, 128, 64, 64, 512
+    say(f"chunked pipeline S={S} chunks [0,{qo}) [{qo},{S})")
+    inp = make_inputs(S, Hq, Hkv, d, index_dim=di, dtype="bf16", seed=7, needles=8)
+    dev = inp.to("cuda")
+
+    def run(p, q, qi, S_):
+        R = p.num_blocks
+        sc = torch.empty(R, S_, device="cuda")
+        B.sp_indexer_scores(p, qi, dev.k_idx[:S_].contiguous(), sc)
+        idx = torch.empty(R, k, dtype=torch.int32, device="cuda")
+        B.sp_topk_select(p, sc, idx)
+        o = torch.empty(p.num_queries, Hq, d, dtype=torch.bfloat16, device="cuda")
+        B.sp_sparse_gqa_attn(p, q, dev.k[:S_].contiguous(), dev.v[:S_].contiguous(), idx, o)
+        return idx, o
+
+    whole = B.Problem(S, Hq, Hkv, d, index_dim=di, topk=k, block_q=b)
+    idx_w, o_w = run(whole, dev.q, dev.q_idx, S)
+    first = B.Problem(qo, Hq, Hkv, d, index_dim=di, topk=k, block_q=b)
+    idx_1, o_1 = run(first, dev.q[:qo].contiguous(), dev.q_idx[:qo].contiguous(), qo)
+    second = B.Problem(S, Hq, Hkv, d, index_dim=di, topk=k, block_q=b, q_offset=qo)
+    idx_2, o_2 = run(second, dev.q[qo:].contiguous(), dev.q_idx[qo:].contiguous(), S)
+    lse = torch.empty(S - qo, Hq, device="cuda")
+    o_d = torch.empty(S - qo, Hq, d, dtype=torch.bfloat16, device="cuda")
+    B.sp_dense_attn(second, dev.q[qo:].contiguous(), dev.k, dev.v, o_d, lse)
+    torch.cuda.synchronize()
+    # the same scores and selections, chunk by chunk
+    assert torch.equal(torch.cat([idx_1, idx_2]), idx_w)
+    assert (torch.cat([o_1, o_2]).float() - o_w.float()).abs().max().item() <= 1e-2
+    ref_o, ref_lse = oracle.dense(inp.q, inp.k, inp.v, rows=np.arange(qo, S))
+    assert max_err(o_d.cpu().double().numpy(), ref_o) <= tol_for("bf16")
+    assert max_err(lse.cpu().double().numpy(), ref_lse) <= 1e-4
