@@ -33,7 +33,7 @@ int check_common(const sp_problem *p) {
 }
 
 int check_heads(const sp_problem *p) {
-  if (p->head_dim != 64 && p->head_dim != 128) return SP_ERR_UNSUPPORTED;
+  if (p->head_dim != 64 && p->head_dim != 128 && p->head_dim != 256) return SP_ERR_UNSUPPORTED;
   // K and V rows are addressed with 32-bit byte offsets.
   const int64_t elt = p->dtype == SP_DTYPE_BF16 ? 2 : 4;
   if ((int64_t)p->seq_len * p->num_kv_heads * p->head_dim * elt >= (int64_t(1) << 32))

@@ -165,10 +165,12 @@ hipError_t launch_attn_rowwise(const Prob &p, const void *q, const void *k, cons
                                KvPages pages) {
   if (p.dtype == SP_DTYPE_BF16) {
     if (p.d == 64) return launch_d<bf16, 64>(p, q, k, v, idx, o, lse, st, pages);
-    return launch_d<bf16, 128>(p, q, k, v, idx, o, lse, st, pages);
+    if (p.d == 128) return launch_d<bf16, 128>(p, q, k, v, idx, o, lse, st, pages);
+    return launch_d<bf16, 256>(p, q, k, v, idx, o, lse, st, pages);
   }
   if (p.d == 64) return launch_d<float, 64>(p, q, k, v, idx, o, lse, st, pages);
-  return launch_d<float, 128>(p, q, k, v, idx, o, lse, st, pages);
+  if (p.d == 128) return launch_d<float, 128>(p, q, k, v, idx, o, lse, st, pages);
+  return launch_d<float, 256>(p, q, k, v, idx, o, lse, st, pages);
 }
 
 }  // namespace sp

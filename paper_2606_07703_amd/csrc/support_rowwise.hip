@@ -52,13 +52,17 @@ __global__ __launch_bounds__(kCols) void mass_rowwise_kernel(
     if (s <= t) {
       float pt = 0.f;
       for (int j = j0; j < j0 + nj; ++j) {
-        float kr[D];
-        load_row<D>(k + ((size_t)s * Hkv + j) * D, kr);
+        // the key row in chunks of at most 128 (bounded registers at d = 256)
+        constexpr int CH = D < 128 ? D : 128;
         for (int hh = 0; hh < G; ++hh) {
           const int h = j * G + hh;
           float dot = 0.f;
+          for (int c = 0; c < D; c += CH) {
+            float kr[CH];
+            load_row<CH>(k + ((size_t)s * Hkv + j) * D + c, kr);
 #pragma unroll
-          for (int e = 0; e < D; ++e) dot = fmaf(qs[h * D + e], kr[e], dot);
+            for (int e = 0; e < CH; ++e) dot = fmaf(qs[h * D + c + e], kr[e], dot);
+          }
           pt += exp2f(dot - ls[h]);
         }
       }
@@ -132,9 +136,13 @@ hipError_t launch_mass_rowwise(const Prob &p, const void *q, const void *k, cons
   hipLaunchKernelGGL((mass_rowwise_kernel<T, D>), grid, dim3(kCols), lds, st, p.S, p.Hq,    \
                      p.Hkv, p.G, p.b, p.agg, p.ha, sl2, (const T *)q, (const T *)k, lse, mass)
   if (p.dtype == SP_DTYPE_BF16) {
-    if (p.d == 64) SP_MASS(bf16, 64); else SP_MASS(bf16, 128);
+    if (p.d == 64) SP_MASS(bf16, 64);
+    else if (p.d == 128) SP_MASS(bf16, 128);
+    else SP_MASS(bf16, 256);
   } else {
-    if (p.d == 64) SP_MASS(float, 64); else SP_MASS(float, 128);
+    if (p.d == 64) SP_MASS(float, 64);
+    else if (p.d == 128) SP_MASS(float, 128);
+    else SP_MASS(float, 256);
   }
 #undef SP_MASS
   return hipGetLastError();

@@ -424,3 +424,39 @@ def test_chunked_dense_and_pipeline_equal_whole_sequence():
     ref_o, ref_lse = oracle.dense(inp.q, inp.k, inp.v, rows=np.arange(qo, S))
     assert max_err(o_d.cpu().double().numpy(), ref_o) <= tol_for("bf16")
     assert max_err(lse.cpu().double().numpy(), ref_lse) <= 1e-4
+
+
+# ------------------------------------------------------ d = d_idx = 256 (f3)
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_head_dim_256(dtype):
+    S, Hq, Hkv, d, b, k = 200, 8, 2, 256, 16, 48
+    say(f"head_dim 256 {dtype}")
+    inp = make_inputs(S, Hq, Hkv, d, index_dim=256, dtype=dtype, seed=256, peaked=True,
+                      needles=4)
+    dev = inp.to("cuda")
+    p = B.Problem(S, Hq, Hkv, d, index_dim=256, topk=k, block_q=b, dtype=dtype)
+    o = torch.empty(S, Hq, d, dtype=inp.q.dtype, device="cuda")
+    lse = torch.empty(S, Hq, device="cuda")
+    B.sp_dense_attn(p, dev.q, dev.k, dev.v, o, lse)
+    mass = torch.full((p.num_blocks, S), float("nan"), device="cuda")
+    B.sp_oracle_support(p, dev.q, dev.k, lse, mass)
+    table = make_support(S, b, k, seed=3)
+    o_s = torch.empty_like(o)
+    B.sp_sparse_gqa_attn(p, dev.q, dev.k, dev.v, table.cuda(), o_s)
+    p1 = B.Problem(S, Hq, Hkv, d, index_dim=256, topk=k, block_q=1, dtype=dtype)
+    t1 = make_support(S, 1, k, seed=4)
+    o_q = torch.empty_like(o)
+    B.sp_sparse_gqa_attn(p1, dev.q, dev.k, dev.v, t1.cuda(), o_q)
+    torch.cuda.synchronize()
+    ref_o, ref_lse = oracle.dense(inp.q, inp.k, inp.v)
+    assert max_err(o.cpu().double().numpy(), ref_o) <= tol_for(dtype)
+    assert max_err(lse.cpu().double().numpy(), ref_lse) <= (1e-5 if dtype == "f32" else 1e-4)
+    ref_m = oracle.support_scores("oracle", range(p.num_blocks), b, q=inp.q, k=inp.k)
+    got_m = mass.cpu().double().numpy()
+    for r in range(p.num_blocks):
+        L = min(r * b + b, S)
+        assert max_err(got_m[r, :L], ref_m[r, :L]) <= 1e-4 * np.abs(ref_m[r, :L]).max()
+    assert max_err(o_s.cpu().double().numpy(), oracle.sparse(inp.q, inp.k, inp.v, table, b)) \
+        <= tol_for(dtype)
+    assert max_err(o_q.cpu().double().numpy(), oracle.sparse(inp.q, inp.k, inp.v, t1, 1)) \
+        <= tol_for(dtype)
