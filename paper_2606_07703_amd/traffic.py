@@ -36,6 +36,7 @@ STAGE_KERNEL_FILE = {
     "block64.indexer_scores": "indexer_mfma.hip",
     "block64.topk": "topk.hip",
     "block64.sparse_attn": "sparse_block_mfma.hip",
+    "block64.sparse_attn_paged": "sparse_block_mfma.hip",
     "perquery.indexer_scores": "indexer_mfma.hip",
     "perquery.topk": "topk.hip",
     "perquery.sparse_attn": "sparse_query_mfma.hip",
