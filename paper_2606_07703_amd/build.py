@@ -9,6 +9,7 @@ from __future__ import annotations
 import concurrent.futures as cf
 import glob
 import os
+import re
 import subprocess
 import sys
 
@@ -27,11 +28,15 @@ CFLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
 
-# Per-file additions. The indexer's max reductions run on MFMA outputs that are
-# never NaN for finite inputs; without IEEE mode the compiler drops the
-# quieting pass it otherwise puts before every v_max_f32.
+# Per-file additions. The indexer's and the attention kernels' max reductions
+# run on MFMA outputs that are never NaN for finite inputs (masked scores are
+# -inf); without IEEE mode the compiler drops the quieting pass it otherwise
+# puts before every v_max_f32.
+NO_IEEE = ["-fno-honor-nans", "-mno-amdgpu-ieee"]
 FILE_FLAGS = {
-    "indexer_mfma.hip": ["-fno-honor-nans", "-mno-amdgpu-ieee"],
+    "indexer_mfma.hip": NO_IEEE,
+    "dense_mfma.hip": NO_IEEE,
+    "sparse_block_mfma.hip": NO_IEEE,
 }
 
 
@@ -39,18 +44,41 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
 
 
-def _compile(src: str) -> str:
+# hipcc's per-kernel resource remarks: kernel names and scratch bytes per lane
+RESOURCE_REMARKS = ["-Rpass-analysis=kernel-resource-usage"]
+
+
+def _scratch_kernels(text: str) -> list:
+    """Kernels whose resource remark reports scratch (register spills or
+    private arrays): in the hot loops these cost a memory round trip."""
+    out, name = [], None
+    for ln in text.splitlines():
+        if "Function Name:" in ln:
+            name = ln.split("Function Name:")[1].split("[")[0].strip()
+        elif "ScratchSize [bytes/lane]:" in ln and name:
+            n = int(ln.split("ScratchSize [bytes/lane]:")[1].split("[")[0])
+            if n:
+                out.append((name, n))
+    return out
+
+
+def _compile(src: str) -> tuple:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + CFLAGS + FILE_FLAGS.get(os.path.basename(src), []) + ["-c", src, "-o", obj]
+    cmd = ([HIPCC] + CFLAGS + FILE_FLAGS.get(os.path.basename(src), []) + RESOURCE_REMARKS
+           + ["-c", src, "-o", obj])
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
-    # the host pass does not know the packed-fp32 feature; drop that one warning
-    noise = "is not a recognized feature for this target"
-    msg = "\n".join(ln for ln in (r.stdout + r.stderr).splitlines() if noise not in ln)
+    text = r.stdout + r.stderr
+    # the host pass does not know the packed-fp32 feature; drop that warning
+    # and the resource remarks (summarised by build())
+    noise = ("is not a recognized feature for this target", "remark:", "kernel-resource-usage")
+    context = re.compile(r"^\s*(\d+\s*)?\|")   # source lines and carets quoted by a remark
+    msg = "\n".join(ln for ln in text.splitlines()
+                    if not any(n in ln for n in noise) and not context.match(ln))
     if msg.strip():
         print(msg, file=sys.stderr)
-    return obj
+    return obj, _scratch_kernels(text)
 
 
 def build(verbose: bool = False) -> str:
@@ -58,7 +86,12 @@ def build(verbose: bool = False) -> str:
     srcs = sources()
     jobs = min(len(srcs), int(os.environ.get("MAX_JOBS", "8")))
     with cf.ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
-        objs = list(ex.map(_compile, srcs))
+        results = list(ex.map(_compile, srcs))
+    objs = [o for o, _ in results]
+    scratch = [k for _, ks in results for k in ks]
+    if scratch and verbose:
+        print("kernels using scratch (bytes/lane): " +
+              ", ".join(f"{n} ({b})" for n, b in scratch), file=sys.stderr)
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)

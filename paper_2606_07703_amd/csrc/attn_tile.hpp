@@ -1,26 +1,39 @@
-// Attention tile machinery shared by the MFMA attention kernels.
+// Attention tile pipeline shared by the MFMA attention kernels (dense causal
+// flash attention, Section 3; selection-block-shared sparse attention,
+// Sections 3 and 4.2).
 //
-// A workgroup owns up to 256 query rows ((query, head) pairs of one KV head,
-// 32 per wave) and walks a list of key positions in tiles of 64. For each
-// tile it stages K and V of the KV head in LDS (both row-major, padded rows),
-// plus the tile's positions and their min/max. attn_tile() then updates each
-// lane's online-softmax state: scores are computed transposed, S^T = K Q^T,
-// so lane (g, c16) owns query row c16 of each 16-row tile and holds keys
-// 16*kt + 4g + r; the output is kept transposed too, O^T = V^T P^T, with the
-// V^T operand read straight from the row-major V tile by the gfx950 LDS
-// transpose read (ds_read_b64_tr_b16), so the per-row rescale stays in the
-// lane and no transposed copy of V is ever written.
+// A workgroup owns up to NW*32 query rows ((query, head) pairs of one KV
+// head, 32 per wave) and walks a list of key positions in tiles of 64. Scores
+// are computed transposed, S^T = K Q^T, on v_mfma_f32_32x32x16_bf16: lane
+// (n, h) = (l%32, l/32) owns query row n of its wave and holds 32 of the 64
+// keys of a tile (keys 32kb + 8i + 4h + r), so the row max and row sum need
+// one half-wave swap. The output is kept transposed too, O^T = V^T P^T: the
+// score accumulators, rounded to bf16, are already the B operand of that
+// product, and the V^T operand is read straight from the row-major V tile by
+// the gfx950 LDS transpose read (ds_read_b64_tr_b16).
 //
-// A key at position s contributes to a row of query t only if
-// 0 <= s <= t (the causal mask of Section 3, applied per query as in
-// Section 4.2); any other position (e.g. a -1 sentinel) contributes nothing.
-// A wave skips the mask test on tiles whose positions all lie in
-// [0, first query of the wave].
+// Two-phase schedule. For key tile n a wave runs
+//   M_n (matrix cores): S_n = K_n Q^T, and O += V_{n-1}^T P_{n-1}^T;
+//   V_n (vector units): mask and row maxima of S_n, rescale of O when a row
+//        maximum rises, P_n = exp2(S_n - m) with its row sums, bf16 P_n.
+// The eight waves of a workgroup form two groups with one wave of each on
+// every SIMD; group 1 runs half a step behind group 0, so while one wave of
+// a SIMD issues matrix instructions its partner issues the softmax, and the
+// two pipes overlap without fine-grained interleaving inside a wave. Each
+// half step ends with one workgroup barrier. K tile n and V tile n - 1 stay
+// in LDS for the two half steps in which the groups run M_n; meanwhile every
+// wave loads its share of the next step's tiles straight into the other
+// buffers. Smaller workgroups run M_n and V_n back to back.
+//
+// A key at position s contributes to a row of query t only if 0 <= s <= t
+// (the causal mask of Section 3, applied per query as in Section 4.2); any
+// other position (a -1 sentinel) contributes nothing. Tiles whose positions
+// all lie in [0, first query of the wave] skip the mask.
 //
 // The running row maximum is raised only when a tile's maximum exceeds it by
 // more than 2^kLazy in the exponent base-2 domain; until then the stale
-// maximum is kept (probabilities up to 2^kLazy are exact in fp32 and bf16
-// range), so the output accumulators are rescaled only when it moves.
+// maximum is kept (probabilities up to 2^kLazy are exact in fp32 and within
+// bf16 range), so the accumulators are rescaled only when it moves.
 #pragma once
 
 #include <math.h>
@@ -29,6 +42,15 @@
 #include "mfma.hpp"
 
 namespace sp {
+
+// The attention workgroups fill most of a CU's LDS, so at most two waves
+// share a SIMD; telling the compiler so lets it spend up to 256 registers a
+// wave on operand prefetch instead of trimming for an occupancy it cannot
+// reach.
+#define SP_ATTN_OCCUPANCY __attribute__((amdgpu_waves_per_eu(1, 2)))
+
+// Operand pairs of the matrix phase read ahead of the products.
+constexpr int kMPrefetch = 2;
 
 constexpr int kAttnKT = 64;      // key positions per tile
 constexpr int kAttnQPW = 32;     // query rows per wave
@@ -40,308 +62,457 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 
 template <int D>
 struct AttnLayout {
-  static constexpr int KRB = D * 2 + 16;   // K row bytes: 16 lanes x 16 B on distinct banks
-  static constexpr int VRB = D * 2 + 32;   // V row bytes: conflict-free transpose reads
-  static constexpr int KBYTES = kAttnKT * KRB;
-  static constexpr int VBYTES = kAttnKT * VRB;
-  static constexpr int POS = KBYTES + VBYTES;          // int positions[64], then min, max
-  static constexpr int BUF = POS + kAttnKT * 4 + 16;
-  static constexpr int KS = D / 32;        // k-steps of K Q^T
-  static constexpr int DT = D / 16;        // 16-row tiles of O^T
+  // K and V tiles (64 rows of D bf16) are row-major with padded rows. K row
+  // stride KRB puts the 16 rows of a b128 operand-read phase on distinct
+  // banks; V row stride VRB puts the 4 rows of a transpose-read phase 16
+  // banks apart. Every operand read is then one lane base plus an immediate
+  // offset. A tile is a whole number of 1 KiB chunks (the unit of a
+  // direct-to-LDS load).
+  static constexpr int RB = D * 2;            // bytes of one row in HBM
+  static constexpr int C = D / 8;             // 16-byte columns of a row
+  static constexpr int KSLOTS = C + 1;        // 16-byte slots of a K row
+  static constexpr int VSLOTS = C + 4;        // 16-byte slots of a V row
+  static constexpr int KRB = 16 * KSLOTS;
+  static constexpr int VRB = 16 * VSLOTS;
+  static constexpr int KTILE = kAttnKT * KRB;
+  static constexpr int VTILE = kAttnKT * VRB;
+  static_assert(KTILE % 1024 == 0 && VTILE % 1024 == 0, "tiles are whole chunks");
+  static constexpr int KS = D / 16;   // k-steps of K Q^T
+  static constexpr int DT = D / 32;   // 32-row blocks of O^T
+  // two K buffers, then (when the output is wanted) two V buffers
+  static constexpr int bytes(bool want_v) { return 2 * KTILE + (want_v ? 2 * VTILE : 0); }
 };
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Wait for every outstanding memory operation of this wave. Issued once
-// before a tile loop, it tells the compiler that loads made before the loop
-// (Q fragments, the first tile) are complete, so no wait on them is placed
-// inside the loop, where it would also stall on the next tile's prefetch.
+// before the tile loop, it tells the compiler that loads made before the
+// loop (Q fragments, the first tile) are complete, so no wait on them is
+// placed inside the loop, where it would also stall on the next prefetch.
 __device__ __forceinline__ void drain_memory() { __builtin_amdgcn_s_waitcnt(0); }
 
-// Global -> registers -> LDS staging of one tile of K, V and positions.
-// pos(e) gives the position of tile entry e (0..63), or a negative value.
-template <int D, int NT, bool WANT_V>
-struct KVStage {
+// Combine lane l with lane l ^ 32 (the other half of a query column).
+__device__ __forceinline__ float half_max(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+}
+__device__ __forceinline__ float half_sum(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(a[0]) + __uint_as_float(a[1]);
+}
+
+// LDS read of four ints at LDS byte address a, by inline assembly: the
+// compiler would otherwise wait for every outstanding direct-to-LDS tile
+// load first, although those never write the arrays read this way.
+__device__ __forceinline__ int4 lds_read_i32x4(uint32_t a) {
+  int4 r;
+  asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(r) : "v"(a) : "memory");
+  return r;
+}
+
+// Global -> LDS staging of one tile of K or V rows of KV head j, with no
+// register round trip: a load instruction fills one 1 KiB chunk of the tile
+// (buffer_load_dwordx4 ... lds puts lane L's 16 bytes at byte 16L of it).
+// Lane L of chunk q holds 16-byte slot 64q + L of the padded tile, that is
+// row (64q + L) / SLOTS, column (64q + L) % SLOTS; lanes on padding slots
+// load nothing. The chunks of a tile go to the waves in turn.
+template <int D, int NW, bool IS_V>
+struct TileLoader {
   using L = AttnLayout<D>;
-  static constexpr int PIECES = kAttnKT * D / 8;    // 16-byte pieces of one tile
-  static constexpr int PER = (PIECES + NT - 1) / NT;
-  uint4 kreg[PER];
-  uint4 vreg[WANT_V ? PER : 1];
-  int spos;
+  static constexpr int SLOTS = IS_V ? L::VSLOTS : L::KSLOTS;
+  static constexpr int CHUNKS = (IS_V ? L::VTILE : L::KTILE) / 1024;
+  static constexpr int PER = (CHUNKS + NW - 1) / NW;
 
-  // All positions are resolved before any row load is issued, so the row
-  // loads of a tile go out back to back.
-  template <typename POS>
-  __device__ __forceinline__ void load(const uint16_t *__restrict__ k,
-                                       const uint16_t *__restrict__ v, int S, int Hkv, int j,
-                                       int tid, POS pos) {
-    load_rows(k, v, S, Hkv, j, tid, pos, pos);
-  }
-
-  // As load, with the K/V row of tile entry e given by row(e) (a paged
-  // cache) while pos(e) stays the token position the mask uses; k and v
-  // hold nrows rows of Hkv heads.
-  template <typename POS, typename ROW>
-  __device__ __forceinline__ void load_rows(const uint16_t *__restrict__ k,
-                                            const uint16_t *__restrict__ v, int nrows, int Hkv,
-                                            int j, int tid, POS pos, ROW row) {
-    // Rows are fetched through buffer resources (base and size in SGPRs,
-    // 32-bit byte offsets per lane): one multiply-add per piece instead of
-    // 64-bit address arithmetic. The API keeps k and v below 4 GiB.
-    const uint32_t nbytes = (uint32_t)nrows * Hkv * D * 2;
-    const auto krs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(k), (short)0,
-                                                       nbytes, kBufferDword3);
-    const auto vrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(v), (short)0,
-                                                       nbytes, kBufferDword3);
+  // row(e) gives the row of tile entry e (rows outside [0, nrows) read row
+  // 0; their keys are masked). Rows are fetched through a buffer resource
+  // (base and size in SGPRs, 32-bit byte offsets per lane); the API keeps k
+  // and v below 4 GiB.
+  template <typename ROW>
+  __device__ __forceinline__ static void load(uint32_t tile, const uint16_t *base, int nrows,
+                                              int Hkv, int j, int wave, int lane, ROW row) {
+    const uint32_t nbytes = (uint32_t)nrows * Hkv * L::RB;
+    const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(base), (short)0,
+                                                      nbytes, kBufferDword3);
     uint32_t off[PER];
+    bool data[PER];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = tid + i * NT;
-      const int key = c / (D / 8), col = c % (D / 8);
-      int s = c < PIECES ? row(key) : 0;
+    for (int p = 0; p < PER; ++p) {
+      const int q = wave + p * NW;
+      const int slot = (q < CHUNKS ? q : 0) * 64 + lane;
+      const int r = slot / SLOTS, c = slot % SLOTS;
+      data[p] = c < L::C;
+      int s = row(data[p] ? r : 0);
       s = (s >= 0 && s < nrows) ? s : 0;
-      off[i] = ((uint32_t)s * Hkv + j) * (D * 2) + col * 16;
+      off[p] = ((uint32_t)s * Hkv + j) * L::RB + (data[p] ? c : 0) * 16;
     }
-    if (tid < kAttnKT) spos = pos(tid);
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      if (tid + i * NT < PIECES) {
-        kreg[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(krs, off[i], 0, 0));
-        if constexpr (WANT_V)
-          vreg[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(vrs, off[i], 0, 0));
-      }
-    }
-  }
-
-  // Also publishes min and max of the tile's positions (wave 0 holds them).
-  __device__ __forceinline__ void store(char *buf, int tid) const {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = tid + i * NT;
-      if (c < PIECES) {
-        const int key = c / (D / 8), col = c % (D / 8);
-        sts16(buf + key * L::KRB + col * 16, kreg[i]);
-        if constexpr (WANT_V) sts16(buf + L::KBYTES + key * L::VRB + col * 16, vreg[i]);
-      }
-    }
-    if (tid < kAttnKT) {
-      int *pl = reinterpret_cast<int *>(buf + L::POS);
-      pl[tid] = spos;
-      int mn = spos, mx = spos;
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) {
-        mn = min(mn, __shfl_xor(mn, off, 64));
-        mx = max(mx, __shfl_xor(mx, off, 64));
-      }
-      if (tid == 0) {
-        pl[kAttnKT] = mn;
-        pl[kAttnKT + 1] = mx;
-      }
+    for (int p = 0; p < PER; ++p) {
+      const int q = wave + p * NW;
+      if ((CHUNKS % NW == 0 || q < CHUNKS) && data[p])
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rs, (__attribute__((address_space(3))) void *)(size_t)(tile + q * 1024), 16, off[p],
+            0, 0, 0);
     }
   }
 };
 
-// Per-wave online-softmax state for 2 x 16 query rows.
+// Wait until at most N of this wave's global loads (the direct-to-LDS tile
+// loads, which complete in issue order) are outstanding; a barrier after it
+// publishes the older tiles to the workgroup. expcnt and lgkmcnt are left at
+// their maxima.
+template <int N>
+__device__ __forceinline__ void wait_loads() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
+
+// This lane's query row: Q fragments (B operand of K Q^T), position, head.
+template <int D>
+struct QRow {
+  bf16x8 bq[AttnLayout<D>::KS];
+  int t, head;
+  bool valid;
+};
+
+// Row m of a workgroup (query-major) is query t0 + m/G, head j*G + m%G. Rows
+// past nrows load row 0 of the workgroup and are never written.
+template <int D>
+__device__ __forceinline__ void load_q_row(const uint16_t *__restrict__ q, int Hq, int G, int j,
+                                           int t0, int m, int nrows, int h, QRow<D> &qr) {
+  qr.valid = m < nrows;
+  const int mm = qr.valid ? m : 0;
+  qr.t = t0 + mm / G;
+  qr.head = j * G + mm % G;
+  const uint16_t *qp = q + ((size_t)qr.t * Hq + qr.head) * D + 8 * h;
+#pragma unroll
+  for (int ks = 0; ks < AttnLayout<D>::KS; ++ks) qr.bq[ks] = as_bf16x8(ldg16(qp + 16 * ks));
+}
+
+// Per-wave online-softmax state for 32 query rows.
 template <int D>
 struct AttnState {
-  f32x4 oacc[AttnLayout<D>::DT][2];
-  float m[2];   // running max (base-2 scaled logits), possibly lagging by < kLazy
-  float l[2];   // this lane's share of the row sum (reduce over g at the end)
-  // Row sums taken on the matrix cores (attn_tile MFMA_SUM): a ones A
-  // operand times P^T puts each row's sum in every C row.
-  f32x4 lsum[2];
-  __device__ __forceinline__ void init() {
-    lsum[0] = lsum[1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  f32x16 o[AttnLayout<D>::DT];   // O^T, rows d = 32dt + 8i + 4h + r
+  bf16x8 p[4];                   // P^T of the last softmaxed tile, k-step f: keys 16f..16f+15
+  float m;                       // running max (base-2 scaled logits), may lag by < kLazy
+  float l;                       // this lane's part of the row sum
+};
+
+// This lane's read offsets into a K tile and a V tile. K fragment (kb, ks)
+// of lane (n, h) is row 32kb + n, bytes 32ks + 16h. V^T fragment (f, dt) of
+// lane (grp, c16) reads, by transpose, rows 16f + 4h + c16/4 (then +8),
+// d = 32dt + 16(grp%2) + 4(c16%4) onwards. The parts that depend on kb, ks,
+// f and dt are immediate offsets.
+template <int D>
+struct TileOffsets {
+  using L = AttnLayout<D>;
+  uint32_t k, v;
+  __device__ __forceinline__ void init(int lane) {
+    const int n = lane & 31, h = lane >> 5, c16 = lane & 15, grp = lane >> 4;
+    k = n * L::KRB + h * 16;
+    v = (4 * h + (c16 >> 2)) * L::VRB + 32 * (grp & 1) + 8 * (c16 & 3);
+  }
+};
+
+// Masks scores whose position fails 0 <= s <= t; pos4(e0) returns the
+// positions of tile entries e0..e0+3.
+template <class POS4>
+__device__ __forceinline__ void mask_tile(f32x16 (&s)[2], int t, int h, POS4 pos4) {
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int4 p = pos4(32 * kb + 8 * i + 4 * h);
+      const int pv[4] = {p.x, p.y, p.z, p.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (!(pv[r] >= 0 && pv[r] <= t)) s[kb][4 * i + r] = -INFINITY;
+    }
+}
+
+__device__ __forceinline__ float tile_max(const f32x16 (&s)[2]) {
+  float a = fmaxf(s[0][0], s[1][0]);
+#pragma unroll
+  for (int e = 1; e < 16; ++e) a = fmaxf(a, fmaxf(s[0][e], s[1][e]));
+  return half_max(a);
+}
+
+// P_i = exp2(scale_log2 * S_i - mref), summed into l; WANT_P keeps it in
+// bf16 as the B operand of the next P V product.
+template <int D, bool WANT_P>
+__device__ __forceinline__ void exp_tile(const f32x16 (&s)[2], float scale_log2, float mref,
+                                         AttnState<D> &st) {
+  float sum = 0.f;
+#pragma unroll
+  for (int f = 0; f < 4; ++f) {
+    bf16x8 pf;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float pv = fast_exp2(fmaf(s[f >> 1][8 * (f & 1) + e], scale_log2, -mref));
+      sum += pv;
+      pf[e] = (__bf16)pv;
+    }
+    if constexpr (WANT_P) st.p[f] = pf;
+  }
+  st.l += sum;
+}
+
+// Operand reads of pair IT of m_tile, issued by inline assembly: each
+// product then waits with its own lgkmcnt for exactly the reads it needs (LDS
+// reads complete in order). The compiler cannot prove that these reads miss
+// the tiles the direct-to-LDS loads are filling, and would otherwise wait for
+// every outstanding load before the first read.
+template <int D, int IT>
+__device__ __forceinline__ void m_kread(uint32_t ka, bf16x8 &r) {   // k-step IT/2, key half IT%2
+  using L = AttnLayout<D>;
+  asm volatile("ds_read_b128 %0, %1 offset:%2"
+               : "=v"(r)
+               : "v"(ka), "i"((IT >> 1) * 32 + (IT & 1) * 32 * L::KRB));
+}
+template <int D, int IT>
+__device__ __forceinline__ void m_vread(uint32_t va, bf16x8 &r) {   // k-step IT/DT, d-block IT%DT
+  using L = AttnLayout<D>;
+  constexpr int off = (IT % L::DT) * 64 + (IT / L::DT) * 16 * L::VRB;
+  uint2 lo, hi;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(lo) : "v"(va), "i"(off));
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(hi) : "v"(va), "i"(off + 8 * L::VRB));
+  __builtin_memcpy(&r, &lo, 8);
+  __builtin_memcpy(reinterpret_cast<char *>(&r) + 8, &hi, 8);
+}
+
+// M_n for one wave: S = K_n Q^T (QK) and O += V_{n-1}^T P^T (PV), as one
+// sequence of D/8 (QK, PV) pairs of matrix instructions: 2 KS = 4 DT = D/8,
+// so pair it is QK k-step it/2 of key half it%2 and PV k-step it/DT of
+// d-block it%DT. Alternating the two products keeps six accumulators in
+// flight, and the operand reads run kMPrefetch pairs ahead of the products.
+template <int D, bool QK, bool PV>
+__device__ __forceinline__ void m_tile(uint32_t kt, uint32_t vt, const TileOffsets<D> &to,
+                                       const bf16x8 (&bq)[AttnLayout<D>::KS], f32x16 (&s)[2],
+                                       AttnState<D> &st) {
+  using L = AttnLayout<D>;
+  constexpr int NP = D / 8;
+  if constexpr (QK) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s[kb][e] = 0.f;
+  }
+  const uint32_t ka = kt + to.k, va = vt + to.v;
+  // The counts below assume only these reads are outstanding on the LGKM
+  // counter (scalar loads return out of order): drain it first.
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  // LDS reads per pair: QK 1, PV 2; operands of the next PF pairs are in
+  // flight while a pair's products issue
+  constexpr int RV = PV ? 2 : 0, RP = (QK ? 1 : 0) + RV;
+  constexpr int PF = kMPrefetch;
+  constexpr int NB = PF + 1;
+  bf16x8 kf[NB], vf[NB];
+  static_for<0, PF>([&](auto I) {
+    constexpr int it = decltype(I)::value;
+    if constexpr (QK) m_kread<D, it>(ka, kf[it]);
+    if constexpr (PV) m_vread<D, it>(va, vf[it]);
+  });
+  static_for<0, NP>([&](auto I) {
+    constexpr int it = decltype(I)::value;
+    constexpr int nx = it + PF;   // pair whose reads are issued now
+    if constexpr (nx < NP) {
+      if constexpr (QK) m_kread<D, (nx < NP ? nx : 0)>(ka, kf[nx % NB]);
+      if constexpr (PV) m_vread<D, (nx < NP ? nx : 0)>(va, vf[nx % NB]);
+    }
+    // reads issued after this pair's: those of the next min(PF, NP-1-it) pairs
+    constexpr int later = (NP - 1 - it < PF ? NP - 1 - it : PF) * RP;
+    if constexpr (QK) {
+      asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(kf[it % NB]) : "i"(RV + later));
+      s[it & 1] = mfma32(kf[it % NB], bq[it >> 1], s[it & 1]);
+    }
+    if constexpr (PV) {
+      asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(vf[it % NB]) : "i"(later));
+      st.o[it % L::DT] = mfma32(vf[it % NB], st.p[it / L::DT], st.o[it % L::DT]);
+    }
+  });
+}
+
+template <int D, int NW, bool WANT_O, class Src>
+struct AttnPipe {
+  using L = AttnLayout<D>;
+  // two groups of four waves; wave w runs on SIMD w % 4
+  static constexpr bool kPaired = NW == 8;
+  const Src &src;
+  const uint16_t *k, *v;
+  int kv_rows, Hkv, j, wave, lane, h, wave_tmin, nt, group;
+  float scale_log2;
+  uint32_t lds;   // K tile i at lds + (i % 2) KTILE, V tile i after the two K buffers
+  TileOffsets<D> to;
+  const QRow<D> &qr;
+  AttnState<D> &st;
+  f32x16 s[2];    // S_n between M_n and V_n
+
+  __device__ __forceinline__ AttnPipe(char *lds_, const Src &src_, const uint16_t *k_,
+                                      const uint16_t *v_, int kv_rows_, int Hkv_, int j_,
+                                      float sl2, int wave_tmin_, const QRow<D> &qr_,
+                                      AttnState<D> &st_)
+      : src(src_), k(k_), v(v_), kv_rows(kv_rows_), Hkv(Hkv_), j(j_), wave_tmin(wave_tmin_),
+        nt(__builtin_amdgcn_readfirstlane(src_.ntiles)), scale_log2(sl2), qr(qr_), st(st_) {
+    // wave-uniform values in scalar registers: the loop and the group
+    // branches are then scalar branches
+    wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    lane = threadIdx.x & 63;
+    h = lane >> 5;
+    group = kPaired ? wave >> 2 : 0;
+    lds = (uint32_t)(size_t)(__attribute__((address_space(3))) char *)lds_;
+    to.init(lane);
+  }
+
+  __device__ __forceinline__ uint32_t ktile(int i) const { return lds + (i & 1) * L::KTILE; }
+  __device__ __forceinline__ uint32_t vtile(int i) const {
+    return lds + 2 * L::KTILE + (i & 1) * L::VTILE;
+  }
+
+  // Tiles of step n + 1: K_{n+1} and V_n, each wave its share of the chunks.
+  // Their buffers held K_{n-1} and V_{n-2}, last read in M_{n-1}, before the
+  // barrier that opened step n. Issued at the top of the step: the row
+  // indices are read before the first load.
+  __device__ __forceinline__ void load_next(int n) {
+    if (n + 1 < nt)
+      TileLoader<D, NW, false>::load(ktile(n + 1), k, kv_rows, Hkv, j, wave, lane,
+                                     [&](int e) { return src.row(n + 1, e); });
+    if constexpr (WANT_O)
+      if (n < nt)
+        TileLoader<D, NW, true>::load(vtile(n), v, kv_rows, Hkv, j, wave, lane,
+                                      [&](int e) { return src.row(n, e); });
+  }
+
+  // M_n: QK (n < nt) and PV (n >= 1)
+  template <bool QK, bool PV>
+  __device__ __forceinline__ void phase_m(int n) {
+    m_tile<D, QK, PV && WANT_O>(QK ? ktile(n) : 0, PV ? vtile(n - 1) : 0, to, qr.bq, s, st);
+  }
+
+  // V_n, for 0 <= n < nt
+  __device__ __forceinline__ void phase_v(int n) {
+    if (src.needs_mask(n, wave_tmin))
+      mask_tile(s, qr.t, h, [&](int e0) { return src.pos4(n, e0); });
+    const float mx = tile_max(s) * scale_log2;   // scale > 0 commutes with max
+    const float mold = st.m;
+    const bool raised = mx > mold + kLazy;
+    const float mnew = raised ? mx : mold;
+    const float mref = mnew == -INFINITY ? 0.f : mnew;
+    st.m = mnew;
+    // Rows whose maximum was raised rescale l and O (rare after the first
+    // tile). The branch is per lane: lanes that do not take it are masked,
+    // so O is updated in place on both paths.
+    if (raised) {
+      const float corr = fast_exp2(mold - mref);   // mold = -inf gives 0
+      st.l *= corr;
+      if constexpr (WANT_O) {
+#pragma unroll
+        for (int dt = 0; dt < L::DT; ++dt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) st.o[dt][e] *= corr;
+      }
+    }
+    exp_tile<D, WANT_O>(s, scale_log2, mref, st);
+  }
+
+  __device__ __forceinline__ void end_step() {
+    wait_loads<0>();
+    __syncthreads();
+  }
+
+  __device__ __forceinline__ void run() {
+#pragma unroll
+    for (int dt = 0; dt < L::DT; ++dt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) st.o[dt][e] = 0.f;
+    st.m = -INFINITY;
+    st.l = 0.f;
+    if (nt <= 0) return;
+    TileLoader<D, NW, false>::load(ktile(0), k, kv_rows, Hkv, j, wave, lane,
+                                   [&](int e) { return src.row(0, e); });
+    drain_memory();
+    __syncthreads();
+    // Every step: all waves issue the next step's loads, run their phases
+    // (group 1 half a step behind group 0) and wait for their loads before
+    // the step's last barrier. The first and last steps are peeled so the
+    // loop body has no phase conditions, and each group runs a loop of its
+    // own (same barriers).
+    if (!kPaired) {
+      load_next(0);
+      phase_m<true, false>(0);
+      phase_v(0);
+      end_step();
+#pragma unroll 1
+      for (int n = 1; n < nt; ++n) {
+        load_next(n);
+        phase_m<true, true>(n);
+        phase_v(n);
+        end_step();
+      }
+      phase_m<false, true>(nt);
+    } else if (group == 0) {
+      load_next(0);
+      phase_m<true, false>(0);
+      __syncthreads();
+      phase_v(0);
+      end_step();
+#pragma unroll 1
+      for (int n = 1; n < nt; ++n) {
+        load_next(n);
+        phase_m<true, true>(n);
+        __syncthreads();
+        phase_v(n);
+        end_step();
+      }
+      phase_m<false, true>(nt);
+      __syncthreads();
+      __syncthreads();
+    } else {
+      load_next(0);
+      __syncthreads();
+      phase_m<true, false>(0);
+      end_step();
+#pragma unroll 1
+      for (int n = 1; n < nt; ++n) {
+        load_next(n);
+        phase_v(n - 1);
+        __syncthreads();
+        phase_m<true, true>(n);
+        end_step();
+      }
+      phase_v(nt - 1);
+      __syncthreads();
+      phase_m<false, true>(nt);
+      __syncthreads();
+    }
+  }
+};
+
+// Final normalisation: writes o (bf16, if non-null) and lse (natural log, if
+// non-null) for this lane's row if it is valid. Rows with no usable key get
+// o = 0 and lse = -inf.
+template <int D>
+__device__ __forceinline__ void attn_finish(const AttnState<D> &st, const QRow<D> &qr, int Hq,
+                                            uint16_t *__restrict__ o, float *__restrict__ lse,
+                                            int h) {
+  const float l = half_sum(st.l);
+  if (!qr.valid) return;
+  const size_t row = (size_t)qr.t * Hq + qr.head;
+  if (lse && h == 0) lse[row] = l > 0.f ? (st.m + log2f(l)) * kLn2 : -INFINITY;
+  if (o) {
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    uint16_t *op = o + row * D + 4 * h;
 #pragma unroll
     for (int dt = 0; dt < AttnLayout<D>::DT; ++dt)
 #pragma unroll
-      for (int qc = 0; qc < 2; ++qc) oacc[dt][qc] = f32x4{0.f, 0.f, 0.f, 0.f};
-    m[0] = m[1] = -INFINITY;
-    l[0] = l[1] = 0.f;
-  }
-};
-
-// One tile: scores, mask, online softmax, and (WANT_O) the P V product.
-// wave_tmin is the smallest query of the wave's valid rows. MFMA_SUM (with
-// WANT_O) takes the row sums from the matrix cores, over the same bf16
-// probabilities that weight V; otherwise they are fp32 vector sums (kept
-// where the log-sum-exp is an output).
-template <int D, bool WANT_O, bool MFMA_SUM = false>
-__device__ __forceinline__ void attn_tile(const char *buf, const bf16x8 (&bq)[2][AttnLayout<D>::KS],
-                                          const int (&qt)[2], float scale_log2, int wave_tmin,
-                                          AttnState<D> &st, int g, int c16) {
-  using L = AttnLayout<D>;
-  constexpr int KS = L::KS, DT = L::DT;
-  const char *kl = buf;
-  const char *vl = buf + L::KBYTES;
-  const int *sl = reinterpret_cast<const int *>(buf + L::POS);
-  const bool mask = !(sl[kAttnKT] >= 0 && sl[kAttnKT + 1] <= wave_tmin);
-  f32x4 sacc[4][2];
-#pragma unroll
-  for (int kt = 0; kt < 4; ++kt) {
-#pragma unroll
-    for (int qc = 0; qc < 2; ++qc) sacc[kt][qc] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 a = as_bf16x8(lds16(kl + (kt * 16 + c16) * L::KRB + ks * 64 + g * 16));
-#pragma unroll
-      for (int qc = 0; qc < 2; ++qc) sacc[kt][qc] = mfma16(a, bq[qc][ks], sacc[kt][qc]);
-    }
-  }
-  if (mask) {
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-      const int4 s4 = *reinterpret_cast<const int4 *>(sl + kt * 16 + g * 4);
-      const int sv[4] = {s4.x, s4.y, s4.z, s4.w};
-#pragma unroll
-      for (int qc = 0; qc < 2; ++qc)
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr)
-          if (!(sv[rr] >= 0 && sv[rr] <= qt[qc])) sacc[kt][qc][rr] = -INFINITY;
-    }
-  }
-  bf16x8 pfrag[2][2];
-  bool grew_any = false;
-  float corr[2];
-#pragma unroll
-  for (int qc = 0; qc < 2; ++qc) {
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) tmax = fmaxf(tmax, sacc[kt][qc][rr]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    tmax *= scale_log2;   // scale > 0 commutes with max
-    const float mold = st.m[qc];
-    const bool grow = tmax > mold + kLazy;
-    const float mnew = grow ? tmax : mold;
-    grew_any |= grow;
-    const float mref = mnew == -INFINITY ? 0.f : mnew;
-    corr[qc] = fast_exp2(mold - mref);   // mold = -inf gives 0; unchanged gives 1
-    st.m[qc] = mnew;
-    float psum = 0.f;
-    float pv[4][4];
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        pv[kt][rr] = fast_exp2(fmaf(sacc[kt][qc][rr], scale_log2, -mref));
-        if constexpr (!MFMA_SUM) psum += pv[kt][rr];
-      }
-    if constexpr (!MFMA_SUM) st.l[qc] = st.l[qc] * corr[qc] + psum;
-    if constexpr (WANT_O) {
-#pragma unroll
-      for (int f = 0; f < 2; ++f) {
-        bf16x8 pf;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          pf[e] = (__bf16)pv[2 * f][e];
-          pf[4 + e] = (__bf16)pv[2 * f + 1][e];
-        }
-        pfrag[qc][f] = pf;
-      }
-    }
-  }
-  if constexpr (WANT_O) {
-    if (__any(grew_any)) {
-#pragma unroll
-      for (int qc = 0; qc < 2; ++qc)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr) st.oacc[dt][qc][rr] *= corr[qc];
-      if constexpr (MFMA_SUM) {
-#pragma unroll
-        for (int qc = 0; qc < 2; ++qc)
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr) st.lsum[qc][rr] *= corr[qc];
-      }
-    }
-    if constexpr (MFMA_SUM) {
-      // one MFMA per 32 keys and 16 rows instead of 32 vector adds per tile
-      bf16x8 ones;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
-#pragma unroll
-      for (int qc = 0; qc < 2; ++qc)
-#pragma unroll
-        for (int f = 0; f < 2; ++f) st.lsum[qc] = mfma16(ones, pfrag[qc][f], st.lsum[qc]);
-    }
-    // O^T += V^T P^T. Lane (g, c16) of the V^T fragment needs d = 16dt + c16
-    // and keys 32f + 4g + {0..3} (then +16): each transpose read has the 16
-    // lanes of group g point at rows 32f + 4g + c16/4 (+16), d = 16dt + 4(c16%4).
-    const char *vbase = vl + (g * 4 + (c16 >> 2)) * L::VRB + (c16 & 3) * 8;
-#pragma unroll
-    for (int f = 0; f < 2; ++f) {
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const char *p0 = vbase + (f * 32) * L::VRB + dt * 32;
-        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) v4i16 *)(size_t)(p0));
-        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) v4i16 *)(size_t)(p0 + 16 * L::VRB));
-        bf16x8 a;
-        __builtin_memcpy(&a, &lo, 8);
-        __builtin_memcpy(reinterpret_cast<char *>(&a) + 8, &hi, 8);
-#pragma unroll
-        for (int qc = 0; qc < 2; ++qc) st.oacc[dt][qc] = mfma16(a, pfrag[qc][f], st.oacc[dt][qc]);
-      }
-    }
-  }
-}
-
-// Q fragments (B operand of K Q^T) for this lane's two query rows.
-// Row m (query-major within the workgroup's rows) is query t0 + m/G, head j*G + m%G.
-template <int D>
-__device__ __forceinline__ void load_q_rows(const uint16_t *__restrict__ q, int Hq, int G, int j,
-                                            int t0, int row0, int nrows, int g, int c16,
-                                            bf16x8 (&bq)[2][AttnLayout<D>::KS], int (&qt)[2],
-                                            int (&qh)[2], bool (&qvalid)[2]) {
-#pragma unroll
-  for (int qc = 0; qc < 2; ++qc) {
-    const int m = row0 + qc * 16 + c16;
-    qvalid[qc] = m < nrows;
-    const int mm = qvalid[qc] ? m : 0;
-    qt[qc] = t0 + mm / G;
-    qh[qc] = j * G + mm % G;
-    const uint16_t *qp = q + ((size_t)qt[qc] * Hq + qh[qc]) * D;
-#pragma unroll
-    for (int ks = 0; ks < AttnLayout<D>::KS; ++ks)
-      bq[qc][ks] = as_bf16x8(ldg16(qp + ks * 32 + g * 8));
-  }
-}
-
-// Final normalisation: writes o (bf16, if non-null) and lse (natural log, if
-// non-null) for this lane's valid rows. Rows with no usable key get o = 0
-// and lse = -inf.
-template <int D>
-__device__ __forceinline__ void attn_finish(AttnState<D> &st, const int (&qt)[2],
-                                            const int (&qh)[2], const bool (&qvalid)[2], int Hq,
-                                            uint16_t *__restrict__ o, float *__restrict__ lse,
-                                            int g) {
-#pragma unroll
-  for (int qc = 0; qc < 2; ++qc) {
-    float l = st.l[qc];
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
-    l += st.lsum[qc][0];
-    if (!qvalid[qc]) continue;
-    if (lse && g == 0)
-      lse[(size_t)qt[qc] * Hq + qh[qc]] = l > 0.f ? (st.m[qc] + log2f(l)) * kLn2 : -INFINITY;
-    if (o) {
-      const float inv = l > 0.f ? 1.f / l : 0.f;
-      uint16_t *op = o + ((size_t)qt[qc] * Hq + qh[qc]) * D;
-#pragma unroll
-      for (int dt = 0; dt < AttnLayout<D>::DT; ++dt) {
+      for (int i = 0; i < 4; ++i) {
         uint2 w;
-        w.x = (uint32_t)float_to_bf16(st.oacc[dt][qc][0] * inv) |
-              ((uint32_t)float_to_bf16(st.oacc[dt][qc][1] * inv) << 16);
-        w.y = (uint32_t)float_to_bf16(st.oacc[dt][qc][2] * inv) |
-              ((uint32_t)float_to_bf16(st.oacc[dt][qc][3] * inv) << 16);
-        *reinterpret_cast<uint2 *>(op + dt * 16 + g * 4) = w;
+        w.x = (uint32_t)float_to_bf16(st.o[dt][4 * i] * inv) |
+              ((uint32_t)float_to_bf16(st.o[dt][4 * i + 1] * inv) << 16);
+        w.y = (uint32_t)float_to_bf16(st.o[dt][4 * i + 2] * inv) |
+              ((uint32_t)float_to_bf16(st.o[dt][4 * i + 3] * inv) << 16);
+        *reinterpret_cast<uint2 *>(op + 32 * dt + 8 * i) = w;
       }
-    }
   }
 }
 

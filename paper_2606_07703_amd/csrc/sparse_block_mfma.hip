@@ -11,92 +11,121 @@
 // not once per query. Every query applies its own causal mask to the shared
 // support; sentinels and out-of-range entries contribute nothing, and the
 // order of a support row does not matter.
+//
+// Workgroups are numbered with the KV head fastest: consecutive workgroups go
+// to different XCDs, so with Hkv = 8 each XCD's L2 holds the K/V rows of one
+// head only.
+#include <limits.h>
+
 #include "attn_tile.hpp"
 #include "kernels.hpp"
 
 namespace sp {
 namespace {
 
-constexpr int kMaxSupport = 4096;   // support row cached in LDS
+constexpr int kMaxSupport = 4096;   // support row cached in LDS (a multiple of the tile)
+constexpr int kMaxTiles = kMaxSupport / kAttnKT;
+
+// The usable support entries in LDS: positions (pos), K/V rows (row: the
+// position, or its paged-cache row), and which tiles need the causal mask
+// for this wave (a bit per tile, kept in registers so the softmax phase reads
+// no LDS).
+struct SupportKeys {
+  int ntiles;
+  const int *pos;
+  const int *rows;
+  uint64_t mask_bits;   // bit t: tile t holds a position past the wave's first query or padding
+  __device__ __forceinline__ int row(int tile, int e) const { return rows[tile * kAttnKT + e]; }
+  __device__ __forceinline__ bool needs_mask(int tile, int) const {
+    return (mask_bits >> tile) & 1;
+  }
+  __device__ __forceinline__ int4 pos4(int tile, int e0) const {
+    // read past the direct-to-LDS tile loads in flight (they never write pos)
+    const uint32_t a = (uint32_t)(size_t)(const __attribute__((address_space(3))) int *)pos;
+    return lds_read_i32x4(a + (tile * kAttnKT + e0) * 4);
+  }
+};
 
 template <int D, int NW, bool PAGED>
-__global__ __launch_bounds__(NW * 64) void sparse_block_kernel(
-    int S, int Hq, int Hkv, int G, int b, int kk, size_t gstride, float scale_log2,
+__global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel(
+    int S, int Hq, int Hkv, int G, int b, int kk, int R, size_t gstride, float scale_log2,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const int32_t *__restrict__ idx,
     uint16_t *__restrict__ o, KvPages pages, int qo) {
   // q and o are addressed by position: the host shifts them back by qo rows
   using L = AttnLayout<D>;
   constexpr int NT = NW * 64;
-  __shared__ __align__(16) char lds[2][L::BUF];
-  __shared__ int red_last[NW];
-  __shared__ int ir[kMaxSupport];
+  __shared__ __align__(16) char lds[L::bytes(true)];
+  __shared__ int red_cnt[NW];
+  __shared__ __align__(16) int ir[kMaxSupport];
   // paged cache: the K/V row of each support entry (ir keeps the position)
-  __shared__ int irp[PAGED ? kMaxSupport : 1];
+  __shared__ __align__(16) int irp[PAGED ? kMaxSupport : 1];
+  __shared__ int tkey[kMaxTiles];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int g = lane >> 4, c16 = lane & 15;
-  const int r = blockIdx.x, j = blockIdx.y;   // r counts blocks from the chunk start
+  const int h = lane >> 5, n = lane & 31;
+  const int j = (int)blockIdx.x % Hkv;
+  const int rest = (int)blockIdx.x / Hkv;
+  const int r = rest % R;   // counts blocks from the chunk start
+  const int chunk = rest / R;
   const int t0 = qo + r * b;
   const int t1 = min(t0 + b, S) - 1;
   const int nrows = (t1 - t0 + 1) * G;
-  const int row0 = blockIdx.z * (NW * kAttnQPW) + wave * kAttnQPW;
+  const int row0 = chunk * (NW * kAttnQPW) + wave * kAttnQPW;
 
-  // Cache the support row; tiles end after the last entry any query of the
-  // block can use (any order).
-  int last = -1;
-  for (int c = tid; c < kk; c += NT) {
-    int s = idx[(size_t)j * gstride + (size_t)r * kk + c];
-    if constexpr (PAGED) {
-      const int row = (s >= 0 && s < S) ? pages.row(s) : -1;
-      if (row < 0) s = -1;   // sentinel, or a page outside the cache: skipped
-      irp[c] = row;
+  QRow<D> qr;
+  load_q_row<D>(q, Hq, G, j, t0, row0 + n, nrows, h, qr);
+
+  // Cache the usable entries of the support row (positions 0 <= s <= t1,
+  // on a page inside the cache), compacted to the front in their original
+  // order; sentinels and later positions contribute to no query of the block.
+  // Positions in a row are distinct, so at most t1 + 1 entries remain.
+  int nv = 0;
+  for (int c0 = 0; c0 < kk; c0 += NT) {
+    const int c = c0 + tid;
+    int s = c < kk ? idx[(size_t)j * gstride + (size_t)r * kk + c] : -1;
+    int prow = s;
+    if constexpr (PAGED) prow = (s >= 0 && s <= t1) ? pages.row(s) : -1;
+    const bool use = s >= 0 && s <= t1 && prow >= 0;
+    const uint64_t ball = __ballot(use);
+    const int before = __popcll(ball & ((1ull << lane) - 1));
+    if (lane == 0) red_cnt[wave] = __popcll(ball);
+    __syncthreads();
+    int base = nv;
+    for (int w = 0; w < wave; ++w) base += red_cnt[w];
+    if (use) {
+      ir[base + before] = s;
+      if constexpr (PAGED) irp[base + before] = prow;
     }
-    ir[c] = s;
-    if (s >= 0 && s <= t1) last = c;
-  }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) last = max(last, __shfl_xor(last, off, 64));
-  if (lane == 0) red_last[wave] = last;
-  __syncthreads();
-  last = -1;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) last = max(last, red_last[w]);
-  const int ntiles = (last + kAttnKT) / kAttnKT;
-
-  bf16x8 bq[2][L::KS];
-  int qt[2], qh[2];
-  bool qvalid[2];
-  load_q_rows<D>(q, Hq, G, j, t0, row0, nrows, g, c16, bq, qt, qh, qvalid);
-
-  AttnState<D> st;
-  st.init();
-  KVStage<D, NT, true> stage;
-  auto pos_of = [&](int c0) {
-    return [=](int e) { return c0 + e < kk ? ir[c0 + e] : -1; };
-  };
-  auto row_of = [&](int c0) {
-    return [=](int e) { return c0 + e < kk ? (PAGED ? irp[c0 + e] : ir[c0 + e]) : -1; };
-  };
-  const int kv_rows = PAGED ? pages.num_pages * pages.page_size : S;
-  if (ntiles > 0) {
-    stage.load_rows(k, v, kv_rows, Hkv, j, tid, pos_of(0), row_of(0));
-    stage.store(lds[0], tid);
-  }
-  drain_memory();
-  __syncthreads();
-  const bool live = row0 < nrows;
-  const int wave_tmin = t0 + row0 / G;
-  for (int it = 0; it < ntiles; ++it) {
-    const bool more = it + 1 < ntiles;
-    if (more)
-      stage.load_rows(k, v, kv_rows, Hkv, j, tid, pos_of((it + 1) * kAttnKT),
-                      row_of((it + 1) * kAttnKT));
-    if (live) attn_tile<D, true, true>(lds[it & 1], bq, qt, scale_log2, wave_tmin, st, g, c16);
-    if (more) stage.store(lds[(it + 1) & 1], tid);
+    for (int w = 0; w < NW; ++w) nv += red_cnt[w];
     __syncthreads();
   }
-  if (live) attn_finish<D>(st, qt, qh, qvalid, Hq, o, nullptr, g);
+  const int ntiles = min((t1 + kAttnKT) / kAttnKT, (nv + kAttnKT - 1) / kAttnKT);
+  for (int c = nv + tid; c < ntiles * kAttnKT; c += NT) {
+    ir[c] = -1;
+    if constexpr (PAGED) irp[c] = -1;
+  }
+  __syncthreads();
+  for (int tile = wave; tile < ntiles; tile += NW) {
+    const int s = ir[tile * kAttnKT + lane];
+    int key = s >= 0 ? s : INT_MAX;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) key = max(key, __shfl_xor(key, off, 64));
+    if (lane == 0) tkey[tile] = key;
+  }
+  __syncthreads();
+
+  AttnState<D> st;
+  const int kv_rows = PAGED ? pages.num_pages * pages.page_size : S;
+  const int wave_tmin = t0 + min(row0, nrows - 1) / G;
+  uint64_t mask_bits = 0;
+  for (int tile = 0; tile < ntiles; ++tile)
+    if (tkey[tile] > wave_tmin) mask_bits |= 1ull << tile;
+  const SupportKeys keys{ntiles, ir, PAGED ? irp : ir, mask_bits};
+  AttnPipe<D, NW, true, SupportKeys> pipe(lds, keys, k, v, kv_rows, Hkv, j, scale_log2, wave_tmin,
+                                          qr, st);
+  pipe.run();
+  attn_finish<D>(st, qr, Hq, o, nullptr, h);
 }
 
 template <int D, bool PAGED>
@@ -106,14 +135,14 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
   int nw = (rows + kAttnQPW - 1) / kAttnQPW;
   nw = nw <= 1 ? 1 : nw <= 2 ? 2 : nw <= 4 ? 4 : 8;
   const int chunks = (rows + nw * kAttnQPW - 1) / (nw * kAttnQPW);
-  dim3 grid(p.R, p.Hkv, chunks);
+  dim3 grid(p.R * p.Hkv * chunks);
   const float sl2 = p.scale * kLog2e;
   const size_t shift = (size_t)p.qo * p.Hq * D;   // chunk rows addressed by position
   const uint16_t *qs = (const uint16_t *)q - shift;
   uint16_t *os = (uint16_t *)o - shift;
 #define SP_SB(NW)                                                                            \
   hipLaunchKernelGGL((sparse_block_kernel<D, NW, PAGED>), grid, dim3(NW * 64), 0, st, p.S,  \
-                     p.Hq, p.Hkv, p.G, p.b, p.k, p.idx_group_stride(), sl2,                   \
+                     p.Hq, p.Hkv, p.G, p.b, p.k, p.R, p.idx_group_stride(), sl2,              \
                      qs, (const uint16_t *)k, (const uint16_t *)v, idx, os, pages, p.qo)
   switch (nw) {
     case 1: SP_SB(1); break;
