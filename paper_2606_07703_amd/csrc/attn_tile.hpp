@@ -91,6 +91,15 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // placed inside the loop, where it would also stall on the next prefetch.
 __device__ __forceinline__ void drain_memory() { __builtin_amdgcn_s_waitcnt(0); }
 
+// Ends a phase for v: v is computed before this point and not moved past
+// it. Matrix and vector arithmetic has no memory effects, so without this the
+// compiler may sink a phase's products past the barrier that ends the phase
+// (to their first use in the next one), which breaks the two-group schedule.
+template <class T>
+__device__ __forceinline__ void settle(T &v) {
+  asm volatile("" : "+v"(v));
+}
+
 // Combine lane l with lane l ^ 32 (the other half of a query column).
 __device__ __forceinline__ float half_max(float x) {
   const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
@@ -231,31 +240,41 @@ __device__ __forceinline__ void mask_tile(f32x16 (&s)[2], int t, int h, POS4 pos
     }
 }
 
+// Row maximum over the lane's 32 keys (a balanced tree: the softmax phase
+// runs with no other vector wave on its SIMD to hide dependent latencies),
+// then across the two half-waves.
 __device__ __forceinline__ float tile_max(const f32x16 (&s)[2]) {
-  float a = fmaxf(s[0][0], s[1][0]);
+  float m[16];
 #pragma unroll
-  for (int e = 1; e < 16; ++e) a = fmaxf(a, fmaxf(s[0][e], s[1][e]));
-  return half_max(a);
+  for (int e = 0; e < 16; ++e) m[e] = fmaxf(s[0][e], s[1][e]);
+#pragma unroll
+  for (int w = 8; w > 0; w >>= 1)
+#pragma unroll
+    for (int e = 0; e < w; ++e) m[e] = fmaxf(m[e], m[e + w]);
+  return half_max(m[0]);
 }
 
 // P_i = exp2(scale_log2 * S_i - mref), summed into l; WANT_P keeps it in
 // bf16 as the B operand of the next P V product.
+// The row sum keeps four partial sums (one per k-step) so that its additions
+// do not form one dependent chain.
 template <int D, bool WANT_P>
 __device__ __forceinline__ void exp_tile(const f32x16 (&s)[2], float scale_log2, float mref,
                                          AttnState<D> &st) {
-  float sum = 0.f;
+  float sum[4];
 #pragma unroll
   for (int f = 0; f < 4; ++f) {
     bf16x8 pf;
+    sum[f] = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float pv = fast_exp2(fmaf(s[f >> 1][8 * (f & 1) + e], scale_log2, -mref));
-      sum += pv;
+      sum[f] += pv;
       pf[e] = (__bf16)pv;
     }
     if constexpr (WANT_P) st.p[f] = pf;
   }
-  st.l += sum;
+  st.l += (sum[0] + sum[1]) + (sum[2] + sum[3]);
 }
 
 // Operand reads of pair IT of m_tile, issued by inline assembly: each
@@ -387,6 +406,14 @@ struct AttnPipe {
   template <bool QK, bool PV>
   __device__ __forceinline__ void phase_m(int n) {
     m_tile<D, QK, PV && WANT_O>(QK ? ktile(n) : 0, PV ? vtile(n - 1) : 0, to, qr.bq, s, st);
+    if constexpr (QK) {
+      settle(s[0]);
+      settle(s[1]);
+    }
+    if constexpr (PV && WANT_O) {
+#pragma unroll
+      for (int dt = 0; dt < L::DT; ++dt) settle(st.o[dt]);
+    }
   }
 
   // V_n, for 0 <= n < nt
@@ -413,6 +440,12 @@ struct AttnPipe {
       }
     }
     exp_tile<D, WANT_O>(s, scale_log2, mref, st);
+    if constexpr (WANT_O) {
+#pragma unroll
+      for (int f = 0; f < 4; ++f) settle(st.p[f]);
+    }
+    settle(st.l);
+    settle(st.m);
   }
 
   __device__ __forceinline__ void end_step() {

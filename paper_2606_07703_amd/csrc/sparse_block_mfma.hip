@@ -56,7 +56,7 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel
   using L = AttnLayout<D>;
   constexpr int NT = NW * 64;
   __shared__ __align__(16) char lds[L::bytes(true)];
-  __shared__ int red_cnt[NW];
+  __shared__ int red_cnt[2][NW];
   __shared__ __align__(16) int ir[kMaxSupport];
   // paged cache: the K/V row of each support entry (ir keeps the position)
   __shared__ __align__(16) int irp[PAGED ? kMaxSupport : 1];
@@ -79,26 +79,47 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel
   // Cache the usable entries of the support row (positions 0 <= s <= t1,
   // on a page inside the cache), compacted to the front in their original
   // order; sentinels and later positions contribute to no query of the block.
-  // Positions in a row are distinct, so at most t1 + 1 entries remain.
+  // Positions in a row are distinct, so at most t1 + 1 entries remain. Each
+  // thread takes kEPT consecutive entries per pass (one pass when kk <= 8 NT):
+  // all its loads are in flight together, a wave scan of the per-thread
+  // counts gives the write offsets, and one barrier per pass publishes the
+  // wave totals (double-buffered, so passes need no second barrier).
+  constexpr int kEPT = 8;
   int nv = 0;
-  for (int c0 = 0; c0 < kk; c0 += NT) {
-    const int c = c0 + tid;
-    int s = c < kk ? idx[(size_t)j * gstride + (size_t)r * kk + c] : -1;
-    int prow = s;
-    if constexpr (PAGED) prow = (s >= 0 && s <= t1) ? pages.row(s) : -1;
-    const bool use = s >= 0 && s <= t1 && prow >= 0;
-    const uint64_t ball = __ballot(use);
-    const int before = __popcll(ball & ((1ull << lane) - 1));
-    if (lane == 0) red_cnt[wave] = __popcll(ball);
-    __syncthreads();
-    int base = nv;
-    for (int w = 0; w < wave; ++w) base += red_cnt[w];
-    if (use) {
-      ir[base + before] = s;
-      if constexpr (PAGED) irp[base + before] = prow;
+  for (int c0 = 0, pass = 0; c0 < kk; c0 += NT * kEPT, ++pass) {
+    const int cb = c0 + tid * kEPT;
+    const int32_t *row = idx + (size_t)j * gstride + (size_t)r * kk;
+    int sv[kEPT], pr[kEPT];
+#pragma unroll
+    for (int e = 0; e < kEPT; ++e) sv[e] = cb + e < kk ? row[cb + e] : -1;
+    int cnt = 0;
+#pragma unroll
+    for (int e = 0; e < kEPT; ++e) {
+      pr[e] = sv[e];
+      if constexpr (PAGED) pr[e] = (sv[e] >= 0 && sv[e] <= t1) ? pages.row(sv[e]) : -1;
+      cnt += (sv[e] >= 0 && sv[e] <= t1 && pr[e] >= 0);
     }
-    for (int w = 0; w < NW; ++w) nv += red_cnt[w];
+    int incl = cnt;   // inclusive scan over the lanes of the wave
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += y;
+    }
+    if (lane == 63) red_cnt[pass & 1][wave] = incl;
     __syncthreads();
+    int pos = nv + incl - cnt;
+    for (int w = 0; w < NW; ++w) {
+      const int tw = red_cnt[pass & 1][w];
+      if (w < wave) pos += tw;
+      nv += tw;
+    }
+#pragma unroll
+    for (int e = 0; e < kEPT; ++e)
+      if (sv[e] >= 0 && sv[e] <= t1 && pr[e] >= 0) {
+        ir[pos] = sv[e];
+        if constexpr (PAGED) irp[pos] = pr[e];
+        ++pos;
+      }
   }
   const int ntiles = min((t1 + kAttnKT) / kAttnKT, (nv + kAttnKT - 1) / kAttnKT);
   for (int c = nv + tid; c < ntiles * kAttnKT; c += NT) {
@@ -106,6 +127,7 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel
     if constexpr (PAGED) irp[c] = -1;
   }
   __syncthreads();
+  // per tile: its largest position, or INT_MAX when it holds padding
   for (int tile = wave; tile < ntiles; tile += NW) {
     const int s = ir[tile * kAttnKT + lane];
     int key = s >= 0 ? s : INT_MAX;
@@ -118,9 +140,8 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel
   AttnState<D> st;
   const int kv_rows = PAGED ? pages.num_pages * pages.page_size : S;
   const int wave_tmin = t0 + min(row0, nrows - 1) / G;
-  uint64_t mask_bits = 0;
-  for (int tile = 0; tile < ntiles; ++tile)
-    if (tkey[tile] > wave_tmin) mask_bits |= 1ull << tile;
+  // bit t: tile t needs the causal mask for this wave (ntiles <= 64)
+  const uint64_t mask_bits = __ballot(lane < ntiles && tkey[lane < ntiles ? lane : 0] > wave_tmin);
   const SupportKeys keys{ntiles, ir, PAGED ? irp : ir, mask_bits};
   AttnPipe<D, NW, true, SupportKeys> pipe(lds, keys, k, v, kv_rows, Hkv, j, scale_log2, wave_tmin,
                                           qr, st);
