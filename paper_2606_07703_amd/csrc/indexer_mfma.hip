@@ -72,34 +72,6 @@ __device__ __forceinline__ float agg2(int agg, float a, float b) {
 __device__ __forceinline__ float as_f(uint32_t x) { return __uint_as_float(x); }
 __device__ __forceinline__ uint32_t as_u(float x) { return __float_as_uint(x); }
 
-// Reduce-scatter across the four 16-lane groups of a wave. Every lane holds
-// one partial per column tile; afterwards lane (g, c) holds the reduction over
-// the four groups of column tile owned_ct(g) at column c. Two half-wave swaps
-// and one row swap (gfx950 v_permlane32_swap / v_permlane16_swap) replace the
-// eight cross-lane shuffles a per-tile butterfly would take.
-template <int NCT>
-__device__ __forceinline__ int owned_ct(int g) {
-  return NCT == 4 ? ((g & 1) << 1) | (g >> 1) : g >> 1;
-}
-
-template <class Op>
-__device__ __forceinline__ float reduce_scatter(const float (&v)[4], Op op) {
-  const auto a = __builtin_amdgcn_permlane32_swap(as_u(v[0]), as_u(v[1]), false, false);
-  const auto b = __builtin_amdgcn_permlane32_swap(as_u(v[2]), as_u(v[3]), false, false);
-  const float m01 = op(as_f(a[0]), as_f(a[1]));   // rows 0,1: tile 0; rows 2,3: tile 1
-  const float m23 = op(as_f(b[0]), as_f(b[1]));   // rows 0,1: tile 2; rows 2,3: tile 3
-  const auto c = __builtin_amdgcn_permlane16_swap(as_u(m01), as_u(m23), false, false);
-  return op(as_f(c[0]), as_f(c[1]));
-}
-
-template <class Op>
-__device__ __forceinline__ float reduce_scatter(const float (&v)[2], Op op) {
-  const auto a = __builtin_amdgcn_permlane32_swap(as_u(v[0]), as_u(v[1]), false, false);
-  const float m = op(as_f(a[0]), as_f(a[1]));     // rows 0,1: tile 0; rows 2,3: tile 1
-  const auto c = __builtin_amdgcn_permlane16_swap(as_u(m), as_u(m), false, false);
-  return op(as_f(c[0]), as_f(c[1]));
-}
-
 // MAXPOS: aggregation is max and the scale is non-negative, so scale and
 // ReLU commute with the max: rows are reduced on raw MFMA outputs and only
 // the reduced value is scaled; tiles entirely below a wave's first query
@@ -179,6 +151,19 @@ struct KeyStageT {
   }
 };
 
+// Half-wave combine on 32x32 MFMA outputs: lane l with lane l ^ 32.
+template <class Op>
+__device__ __forceinline__ float half_combine(float x, Op op) {
+  const auto a = __builtin_amdgcn_permlane32_swap(as_u(x), as_u(x), false, false);
+  return op(as_f(a[0]), as_f(a[1]));
+}
+
+// The block kernel runs on v_mfma_f32_32x32x16_bf16 with queries as rows:
+// A = 32 queries x 16 dims (resident in registers), B = 16 dims x 32 keys
+// (a key row read from LDS), so lane (n, h) of a 32x32 score tile holds key
+// column n for queries 8i + 4h + r. A selection block's aggregate is then a
+// lane-local reduction plus one half-wave combine, and the half index h picks
+// which key tile or block a lane stores, so every store row is contiguous.
 template <int DI, int BQ, bool MAXPOS, int NW, int KC>
 __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_items, int g0,
                                                                 int agg, int relu, float scale,
@@ -187,7 +172,7 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_ite
                                                                 float *__restrict__ Y) {
   using T = BlockTile<DI>;
   constexpr int NT = NW * 64;
-  constexpr int KT = T::KT, RB = T::RB, KS = DI / 32, NSUB = T::NSUB, PD = T::PD, NB = T::NB;
+  constexpr int KT = T::KT, RB = T::RB, KS = DI / 16, NSUB = T::NSUB, PD = T::PD, NB = T::NB;
   constexpr int QG = NW * kQW;
   static_assert(KC % QG == 0 || QG % KC == 0, "chunk and query group sizes must nest");
   static_assert(KC % KT == 0, "chunks hold whole tiles");
@@ -195,7 +180,7 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_ite
   __shared__ float red[NW / 2][KT];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int g = lane >> 4, c16 = lane & 15;
+  const int n = lane & 31, h = lane >> 5;
   int qg, kc;
   decode_item<QG, KC>(blockIdx.x, n_items, S, g0, qg, kc);
   const int q0 = qg * QG;
@@ -205,16 +190,16 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_ite
   const int ntiles = (k_end - k_begin + KT - 1) / KT;
   const int qw0 = q0 + wave * kQW;
   const int qw_last = min(qw0 + kQW, S) - 1;  // < qw0 when the wave is past the end
-  // key column (within a 64-key sub-tile) this lane holds after the reduce-scatter
-  const int my_col = owned_ct<4>(g) * 16 + c16;
 
-  bf16x8 a[4][KS];
+  // A operands: query tile qt (32 queries), k-step ks: row qw0 + 32qt + n,
+  // dims 16ks + 8h .. + 7
+  bf16x8 a[2][KS];
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt) {
-    const int row = min(qw0 + rt * 16 + c16, S - 1);
+  for (int qt = 0; qt < 2; ++qt) {
+    const int row = min(qw0 + qt * 32 + n, S - 1);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      a[rt][ks] = as_bf16x8(ldg16(qi + (size_t)row * DI + ks * 32 + g * 8));
+      a[qt][ks] = as_bf16x8(ldg16(qi + (size_t)row * DI + ks * 16 + h * 8));
   }
 
   KeyStageT<DI, KT, RB, NT> stage[PD];
@@ -227,66 +212,113 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_ite
   const float neutral = agg == SP_AGG_MAX ? -INFINITY : 0.f;
   auto op = [agg](float x, float y) { return MAXPOS ? fmaxf(x, y) : agg2(agg, x, y); };
   constexpr int BPW = BQ >= kQW ? 1 : kQW / BQ;   // blocks per wave
-  constexpr int RPB = BQ >= kQW ? 4 : BQ / 16;    // row tiles per block
+  // values a lane keeps per 64-key sub-tile: BPW = 1: the key tile ct = h;
+  // BPW >= 2: for each key tile, the blocks bb = h, h + 2, ...
+  constexpr int NV = BPW == 1 ? 1 : BPW;
 
-  // One 64-key sub-tile: scores of the wave's 64 queries, masked unless FULL
-  // (every pair causal and valid), reduced per selection block; returns the
-  // reduction for key column my_col in out[bb].
-  auto subtile = [&](const char *cur, int sb, int ks0, float (&out)[BPW], auto full_) {
+  // One 64-key sub-tile (key tiles ct = 0, 1 of 32 keys): scores of the
+  // wave's 64 queries, masked unless FULL (every pair causal and valid),
+  // aggregated per selection block. out[v] is the value for key
+  // ks0 + 32 ct(v) + n of block bb(v).
+  auto subtile = [&](const char *cur, int sb, int ks0, float (&out)[NV], auto full_) {
     constexpr bool FULL = decltype(full_)::value;
-    float part[BPW][4];
+    f32x16 acc[2][2];
+    // aggregate of key tile ct per selection block, kept in out[] (see above)
+    auto reduce_key_tile = [&](int ct) {
+      const int s = ks0 + ct * 32 + n;
+      float vals[BPW];
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) {
-      const int s = ks0 + ct * 16 + c16;
-      const char *krow = cur + (sb * 64 + ct * 16 + c16) * RB + g * 16;
-      f32x4 acc[4];
+      for (int bb = 0; bb < BPW; ++bb) vals[bb] = neutral;
 #pragma unroll
-      for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 b = as_bf16x8(lds16(krow + ks * 64));
+        for (int i = 0; i < 4; ++i) {
+          float x[4];
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) acc[rt] = mfma16(a[rt][ks], b, acc[rt]);
-      }
-#pragma unroll
-      for (int bb = 0; bb < BPW; ++bb) part[bb][ct] = neutral;
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt) {
-        float x[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          x[r] = acc[rt][r];
-          if constexpr (!MAXPOS) {
-            x[r] *= scale;
-            if (relu) x[r] = fmaxf(x[r], 0.f);
+          for (int r = 0; r < 4; ++r) {
+            x[r] = acc[ct][qt][4 * i + r];
+            if constexpr (!MAXPOS) {
+              x[r] *= scale;
+              if (relu) x[r] = fmaxf(x[r], 0.f);
+            }
+            if constexpr (!FULL) {
+              const int t = qw0 + qt * 32 + i * 8 + h * 4 + r;
+              if (!(t <= qw_last && s <= t)) x[r] = neutral;
+            }
           }
-          if constexpr (!FULL) {
-            const int t = qw0 + rt * 16 + g * 4 + r;
-            if (!(t <= qw_last && s <= t)) x[r] = neutral;
-          }
+          // block of query rows 32qt + 8i + 4h + r (a block never splits an 8-row group)
+          const int bb = BPW == 1 ? 0 : (qt * 32 + i * 8) / BQ;
+          vals[bb] = op(vals[bb], op(op(x[0], x[1]), op(x[2], x[3])));
         }
-        const float m = op(op(x[0], x[1]), op(x[2], x[3]));
-        part[rt / RPB][ct] = op(part[rt / RPB][ct], m);
-      }
-    }
 #pragma unroll
-    for (int bb = 0; bb < BPW; ++bb) {
-      float m = reduce_scatter(part[bb], op);
-      if constexpr (MAXPOS) {
-        m *= scale;
-        if (relu) m = fmaxf(m, 0.f);   // -inf (no causal row) becomes 0; never stored
+      for (int bb = 0; bb < BPW; ++bb) {
+        float m = half_combine(vals[bb], op);
+        if constexpr (MAXPOS) {
+          m *= scale;
+          if (relu) m = fmaxf(m, 0.f);   // -inf (no causal row) becomes 0; never stored
+        }
+        vals[bb] = m;
       }
-      out[bb] = m;
+      if constexpr (BPW == 1) {
+        if (ct == 0) out[0] = vals[0];
+        else out[0] = h ? vals[0] : out[0];
+      } else {
+#pragma unroll
+        for (int m = 0; m < BPW / 2; ++m) out[ct * (BPW / 2) + m] = h ? vals[2 * m + 1] : vals[2 * m];
+      }
+    };
+    // key tiles multiplied together: both (four accumulator chains), or one
+    // at a time when the 256-dim query operands leave no room
+    constexpr int CTP = DI <= 128 ? 2 : 1;
+    const char *krow = cur + (sb * 64 + n) * RB + h * 16;
+#pragma unroll
+    for (int c0 = 0; c0 < 2; c0 += CTP) {
+#pragma unroll
+      for (int ct = c0; ct < c0 + CTP; ++ct)
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[ct][qt][e] = 0.f;
+      // reads of key fragment (ks, ct) run two steps ahead of its products
+      // (inline reads with their own lgkmcnt waits; LDS reads complete in order)
+      constexpr int NR = KS * CTP, PF = 2, NBF = PF + 1;
+      bf16x8 kb[NBF];
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      static_for<0, NR + PF>([&](auto I) {
+        constexpr int x = decltype(I)::value;
+        if constexpr (x < NR) {   // issue read x
+          constexpr int ks = x / CTP, cc = x % CTP;
+          asm volatile("ds_read_b128 %0, %1 offset:%2"
+                       : "=v"(kb[x % NBF])
+                       : "v"((uint32_t)(size_t)(const __attribute__((address_space(3))) char *)krow),
+                         "i"((c0 + cc) * 32 * RB + ks * 32));
+        }
+        if constexpr (x >= PF) {   // products of read x - PF
+          constexpr int y = x - PF, ks = y / CTP, ct = y % CTP;
+          constexpr int later = (NR - 1 - y < PF ? NR - 1 - y : PF);
+          asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(kb[y % NBF]) : "i"(later));
+#pragma unroll
+          for (int qt = 0; qt < 2; ++qt)
+            acc[c0 + ct][qt] = mfma32(a[qt][ks], kb[y % NBF], acc[c0 + ct][qt]);
+        }
+      });
+      if constexpr (CTP == 1) reduce_key_tile(c0);
+    }
+    if constexpr (CTP == 2) {
+      reduce_key_tile(0);
+      reduce_key_tile(1);
     }
   };
+  // key (within a 64-key sub-tile) and block of kept value v
+  auto v_key = [&](int v) { return BPW == 1 ? 32 * h + n : 32 * (v / (BPW / 2)) + n; };
+  auto v_block = [&](int v) { return BPW == 1 ? 0 : 2 * (v % (BPW / 2)) + h; };
 
   auto tile = [&](int it, auto j_) {
     constexpr int j = decltype(j_)::value;   // it % PD
     const int kt0 = k_begin + it * KT;
     if (it + PD < ntiles) stage[j].load(ki, S, kt0 + PD * KT, tid);
     const char *cur = lds[it % NB];
-    // out[sb][bb]: aggregate over the queries of block bb, key kt0 + 64 sb + my_col
-    float out[NSUB][BPW];
+    float out[NSUB][NV];
     // (DI = 256 keeps one code path: its 128 query registers leave no room
     // for two instantiations of the sub-tile)
     if (DI <= 128 && kt0 + KT - 1 <= qw0 && qw0 + kQW - 1 <= qw_last) {
@@ -302,26 +334,25 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_ite
       for (int sb = 0; sb < NSUB; ++sb) {
         const int ks0 = kt0 + sb * 64;
 #pragma unroll
-        for (int bb = 0; bb < BPW; ++bb) out[sb][bb] = neutral;
+        for (int v = 0; v < NV; ++v) out[sb][v] = neutral;
         if (ks0 <= qw_last) subtile(cur, sb, ks0, out[sb], std::false_type{});
       }
     }
     if constexpr (BQ <= kQW) {
 #pragma unroll
-      for (int sb = 0; sb < NSUB; ++sb) {
-        const int s = kt0 + sb * 64 + my_col;
+      for (int sb = 0; sb < NSUB; ++sb)
 #pragma unroll
-        for (int bb = 0; bb < BPW; ++bb) {
-          const int tb0 = qw0 + bb * BQ;                  // first query of the block
+        for (int v = 0; v < NV; ++v) {
+          const int s = kt0 + sb * 64 + v_key(v);
+          const int tb0 = qw0 + v_block(v) * BQ;          // first query of the block
           const int tb1 = min(tb0 + BQ, S) - 1;
-          if (tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = out[sb][bb];
+          if (tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = out[sb][v];
         }
-      }
     } else {
       // BQ = 128: waves 2i and 2i+1 hold the two halves of one block.
       if (wave & 1) {
 #pragma unroll
-        for (int sb = 0; sb < NSUB; ++sb) red[wave >> 1][sb * 64 + my_col] = out[sb][0];
+        for (int sb = 0; sb < NSUB; ++sb) red[wave >> 1][sb * 64 + v_key(0)] = out[sb][0];
       }
       __syncthreads();
       if (!(wave & 1)) {
@@ -329,8 +360,8 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_ite
         const int tb1 = min(tb0 + BQ, S) - 1;
 #pragma unroll
         for (int sb = 0; sb < NSUB; ++sb) {
-          const int s = kt0 + sb * 64 + my_col;
-          const float m = op(out[sb][0], red[wave >> 1][sb * 64 + my_col]);
+          const int s = kt0 + sb * 64 + v_key(0);
+          const float m = op(out[sb][0], red[wave >> 1][sb * 64 + v_key(0)]);
           if (tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = m;
         }
       }
