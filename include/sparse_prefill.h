@@ -6,9 +6,9 @@
  * prefill path of "How Much Dense Attention is Necessary? Oracle-Guided
  * Sparse Prefill for Full/GQA Layers in Hybrid Long-Context Models":
  *
- *   indexer mode (Algorithm 2, steps 4-5):
+ *   indexer mode (Algorithm 2, scoring, selection and sparse prefill):
  *     sp_indexer_scores -> sp_topk_select -> sp_sparse_gqa_attn
- *   oracle mode (Algorithm 1, steps 2-5):
+ *   oracle mode (Algorithm 1, dense pass, selection and restricted recomputation):
  *     sp_dense_attn (normalisers) -> sp_oracle_support -> sp_topk_select
  *     -> sp_sparse_gqa_attn
  *   dense baseline (Section 3):
@@ -125,7 +125,7 @@ typedef struct sp_problem {
 } sp_problem;
 
 /*
- * Dense causal GQA attention (Section 3, first equation; Algorithm 1 step 2).
+ * Dense causal GQA attention (Section 3, first equation; Algorithm 1, dense scores and normalisers).
  *   o[t,h]   = sum_{s<=t} softmax_{s'<=t}(attn_scale * <q[t,h], k[s',g(h)]>)_s v[s,g(h)]
  *   lse[t,h] = log sum_{s<=t} exp(attn_scale * <q[t,h], k[s,g(h)]>)
  * o may be NULL when lse is given: only the softmax normalisers are
@@ -138,7 +138,7 @@ int sp_dense_attn(const sp_problem *p, const void *q, const void *k, const void 
 
 /*
  * Attention-mass oracle scores (Section 4.1 head-averaged mass; Section 4.2
- * block max; Algorithm 1 step 3):
+ * block max; Algorithm 1, head-averaged probabilities):
  *   P_t(s)    = (1/Hq) sum_h exp(attn_scale * <q[t,h], k[s,g(h)]> - lse[t,h]),  s <= t
  *   mass[r,s] = AGG_{t in block r, t >= s} P_t(s),  s <= t1_r
  * lse must come from sp_dense_attn on the same q, k and problem. AGG is
@@ -150,20 +150,20 @@ int sp_oracle_support(const sp_problem *p, const void *q, const void *k, const f
                       float *mass, hipStream_t stream);
 
 /*
- * Head-collapsed indexer scores (Section 6.3 equation for z; Algorithm 2
- * step 4):
+ * Head-collapsed indexer scores (Section 6.3 equation for z; Algorithm 2,
+ * candidate scoring):
  *   z[t,s]      = ReLU(index_scale * <q_idx[t], k_idx[s]>),  s <= t  (no ReLU if relu=0)
  *   scores[r,s] = AGG_{t in block r, t >= s} z[t,s],  s <= t1_r
  * q_idx/k_idx are the indexer vectors after key normalisation, RoPE and
- * any query scale (Algorithm 2 step 3).
+ * any query scale (Algorithm 2, query scale).
  */
 int sp_indexer_scores(const sp_problem *p, const void *q_idx, const void *k_idx,
                       float *scores, hipStream_t stream);
 
 /*
- * Top-k support selection (Section 4.1 TopK; Section 4.2; Algorithm 1
- * steps 4-5; Algorithm 2 step 5). For block r with L = t1_r+1 causal
- * positions:
+ * Top-k support selection (Section 4.1 TopK; Section 4.2; Algorithm 1,
+ * selection and restricted recomputation; Algorithm 2, selection and sparse
+ * GQA prefill). For block r with L = t1_r+1 causal positions:
  *   L <= k : idx[r] = 0..L-1, then -1;
  *   L >  k : the Wf = min(local_window, k) positions t1_r-Wf+1..t1_r are
  *            forced; the other k-Wf are the first positions of 0..L-Wf-1
@@ -178,7 +178,7 @@ int sp_topk_select(const sp_problem *p, const float *scores, int32_t *idx, void 
 
 /*
  * Sparse GQA attention over the shared supports (Section 3, second
- * equation; Section 4.2 per-query causal mask; Algorithm 1 step 5).
+ * equation; Section 4.2 per-query causal mask; Algorithm 1, restricted recomputation).
  * Query t of block r = t/b, head h, uses U = { s in idx[r,:] : 0 <= s <= t }:
  *   o[t,h] = sum_{s in U} softmax_U(attn_scale * <q[t,h], k[s,g(h)]>)_s v[s,g(h)]
  * and o[t,h] = 0 when U is empty. Entries < 0 or >= S are skipped (they are
@@ -209,7 +209,7 @@ int sp_sparse_gqa_attn_paged(const sp_problem *p, const void *q, const void *k_p
 
 /*
  * Fused per-query indexer scoring and top-k (Section 6.3 score equation;
- * Section 6.4 fused path and Algorithm 2 steps 4-5 with b_sel = 1; Section 4.1
+ * Section 6.4 fused path and Algorithm 2, scoring, selection and sparse prefill with b_sel = 1; Section 4.1
  * TopK): idx[t,:] = the top-k positions of z[t,s] = ReLU?(index_scale *
  * <q_idx[t], k_idx[s]>) over s <= t, selected exactly as sp_topk_select does
  * on those scores (forced window of min(W,k) most recent positions, then
@@ -229,7 +229,7 @@ int sp_indexer_topk(const sp_problem *p, const void *q_idx, const void *k_idx, i
 
 /*
  * Head-collapsed indexer front end (Section 6.3, the projection equations
- * and the score equation's RoPE; Algorithm 2 steps 2-3): for token t at
+ * and the score equation's RoPE; Algorithm 2, indexer projection and its key normalisation, RoPE and query scale): for token t at
  * position pos0 + t, with x_t = x[t,:],
  *   q_idx[t] = RoPE(W_Q x_t, pos0 + t),
  *   k_idx[t] = RoPE(LN(W_K x_t), pos0 + t),

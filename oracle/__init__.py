@@ -10,12 +10,12 @@ in the paper's order:
 
 * oracle mode (Algorithm 1): dense normalisers -> head-averaged mass P ->
   block aggregation -> top-k -> restricted attention;
-* indexer mode (Algorithm 2, steps 4-5): indexer scores -> block aggregation
+* indexer mode (Algorithm 2, scoring, selection and sparse prefill): indexer scores -> block aggregation
   -> top-k -> restricted attention;
 * dense attention (Section 3);
 * the KL distillation objective and its gradient (Section 6.2);
 * the head-collapsed indexer front end: projection, key LayerNorm, RoPE
-  (Section 6.3, Algorithm 2 steps 2-3).
+  (Section 6.3, Algorithm 2, indexer projection and its key normalisation, RoPE and query scale).
 
 Parity pins for every function live in ``tests/test_oracle_pins.py``.
 """
@@ -163,7 +163,7 @@ def aggregate(X: np.ndarray, trows, agg: str = "max") -> np.ndarray:
 
 
 def topk(Y: np.ndarray, lens, k: int, window: int = 0) -> np.ndarray:
-    """Top-k supports of score rows Y [n,>=max(lens)] (Section 4.1, Algorithm 1 steps 4-5)."""
+    """Top-k supports of score rows Y [n,>=max(lens)] (Section 4.1, Algorithm 1, selection and restricted recomputation)."""
     Y = _f64(np.atleast_2d(Y))
     lens = _i32(np.atleast_1d(lens))
     out = np.full((len(lens), k), -1, dtype=np.int32)
@@ -235,7 +235,7 @@ def kl(P, z, rows):
 
 def project(x, wq, wk, gamma, beta, rows=None, pos0: int = 0, theta: float = 10000.0,
             eps: float = 1e-6):
-    """Indexer front end (Section 6.3; Algorithm 2 steps 2-3).
+    """Indexer front end (Section 6.3; Algorithm 2, indexer projection and its key normalisation, RoPE and query scale).
 
     x [S,dm], wq/wk [d_idx,dm], gamma/beta [d_idx]. Returns (q_idx, k_idx),
     each [n,d_idx]: RoPE(W_Q x_t) and RoPE(LN(W_K x_t)) at positions pos0 + t.
@@ -258,9 +258,9 @@ def support_scores(mode: str, units: Sequence[int], block_q: int, *, q=None, k=N
                    index_scale=None, relu: bool = True, group: Optional[int] = None) -> np.ndarray:
     """Aggregated score rows Y [len(units), S] for selection blocks ``units``.
 
-    mode "oracle": X = head-averaged mass P (Algorithm 1 steps 2-3), over the
+    mode "oracle": X = head-averaged mass P (Algorithm 1, normalisers and head-averaged probabilities), over the
     heads of KV group ``group`` when given (per-group support);
-    mode "indexer": X = indexer scores z (Algorithm 2 step 4).
+    mode "indexer": X = indexer scores z (Algorithm 2, candidate scoring).
     Then Y = block aggregate of X (identity when block_q == 1).
     """
     S = (q if mode == "oracle" else q_idx).shape[0]

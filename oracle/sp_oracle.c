@@ -51,7 +51,7 @@ static double log_normaliser(const double *l, int n) {
  * Dense causal GQA attention (Section 3, first equation):
  *   A[t,h,s] = softmax_{s'<=t}(<q_{t,h}, k_{s',g(h)}> * scale)_s
  *   o[t,h]   = sum_{s<=t} A[t,h,s] v_{s,g(h)}
- * plus the normaliser lse[t,h] = log sum_{s<=t} exp(l) (Algorithm 1, step 2).
+ * plus the normaliser lse[t,h] = log sum_{s<=t} exp(l) (Algorithm 1, dense scores and normalisers).
  * rows[i] is a query position; o is [nrows,Hq,d], lse [nrows,Hq] (either may
  * be NULL).
  */
@@ -88,7 +88,7 @@ void orc_dense(int S, int Hq, int Hkv, int d, double scale, const double *q,
 /*
  * Head-averaged attention mass (Section 4.1):
  *   P_t(s) = (1/Hq) sum_h A[t,h,s],  s <= t.
- * Following Algorithm 1 steps 2-3: the normaliser of every head is computed
+ * Following Algorithm 1, normalisers and head-averaged probabilities: the normaliser of every head is computed
  * first, then the probabilities are reconstructed and averaged over heads.
  * The average runs over the heads [h0, h0 + nh): all Hq heads for the
  * head-averaged token support S_t, or the G heads of KV group r for the
@@ -183,8 +183,8 @@ static int cand_cmp(const void *a, const void *b) {
 }
 
 /*
- * Top-k support of one score row (Section 4.1 TopK; Algorithm 1 step 4 and
- * the sentinel padding of step 5). For row i with L = lens[i] valid positions
+ * Top-k support of one score row (Section 4.1 TopK; Algorithm 1, top-k
+ * selection and the sentinel padding of the restricted recomputation). For row i with L = lens[i] valid positions
  * 0..L-1:
  *   - if L <= k every valid position is taken;
  *   - else the Wf = min(W, k) most recent positions are forced, and the
@@ -312,7 +312,7 @@ void orc_kl(int S, int n, const int32_t *rows, const double *P, const double *z,
 
 /*
  * Head-collapsed indexer front end (Section 6.3, first two equations;
- * Algorithm 2 steps 2-3), for token rows t = rows[i] at positions pos0 + t:
+ * Algorithm 2, indexer projection and its key normalisation, RoPE and query scale), for token rows t = rows[i] at positions pos0 + t:
  *   q = W_Q x_t,   k = LN(W_K x_t),
  *   LN(a) = (a - mean(a)) / sqrt(var(a) + eps) * gamma + beta   (over d_idx),
  *   q_idx = RoPE(q, pos0 + t),   k_idx = RoPE(k, pos0 + t),

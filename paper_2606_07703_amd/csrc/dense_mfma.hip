@@ -1,5 +1,5 @@
 // Dense causal GQA attention on bf16 MFMA (Section 3, first equation;
-// Algorithm 1 step 2): a flash-attention forward that also returns the
+// Algorithm 1, dense scores and normalisers): a flash-attention forward that also returns the
 // softmax normaliser lse[t,h] = log sum_{s<=t} exp(scale <q[t,h], k[s,g(h)]>).
 //
 // One workgroup per (tile of 256/G queries, KV head j): its 256 query rows are

@@ -1,12 +1,14 @@
-// Head-collapsed indexer scores on bf16 MFMA (Section 6.3; Algorithm 2 step 4).
+// Head-collapsed indexer scores on bf16 MFMA (Section 6.3; Algorithm 2, candidate scoring).
 //
 //   z[t,s] = ReLU(iscale * <q_idx[t], k_idx[s]>),  s <= t
 //
 // Two kernels share one structure: a workgroup owns a range of queries
-// (64 per wave, resident in registers as MFMA operands) and a chunk of up to
-// 1024 keys, which it streams through double-buffered LDS tiles. Each key
-// tile is read from L2 once per workgroup and reused by every wave. Only key
-// tiles at or below a wave's last query are multiplied (causal skipping).
+// (64 per wave, resident in registers as MFMA operands) and streams key
+// tiles through double-buffered LDS. Each key tile is read from L2 once per
+// workgroup and reused by every wave. Only key tiles at or below a wave's
+// last query are multiplied (causal skipping). The rows kernel gives each
+// workgroup a chunk of up to 1024 keys; the block kernel runs a persistent
+// grid over (query group, key tile) units, split evenly between workgroups.
 //
 // * indexer_block_kernel (b in {16, 32, 64, 128}): the epilogue scales,
 //   applies the ReLU and the per-pair causal mask (t >= s, Section 4.2) and
@@ -16,6 +18,9 @@
 //   issued with keys as rows (scores transposed) so that each lane holds
 //   four consecutive keys of one query and writes them as one 16-byte store.
 #include <math.h>
+
+#include <atomic>
+#include <climits>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -76,51 +81,57 @@ __device__ __forceinline__ uint32_t as_u(float x) { return __float_as_uint(x); }
 // ReLU commute with the max: rows are reduced on raw MFMA outputs and only
 // the reduced value is scaled; tiles entirely below a wave's first query
 // skip the causal test.
-// Work items of the block kernel are the causal (query group, key chunk)
-// pairs: chunk kc (keys kc*KC ..) meets query groups qg >= kc*KC/QG. Items are
-// numbered by chunk, so neighbouring items share their key chunk, and
-// workgroup i (which the hardware places on XCD i % 8) takes item
-// xcd_range_start + i / 8: each XCD walks a contiguous run of items and its L2
-// sees each key chunk once for several query groups.
-// g0: first query group (a chunk starting at g0 * QG covers groups g0 ..).
-template <int QG, int KC>
-__device__ __forceinline__ void decode_item(int i, int n_items, int S, int g0, int &qg,
-                                            int &kc) {
-  const int x = i % kXcds, j = i / kXcds;
-  const int lin = x * (n_items / kXcds) + min(x, n_items % kXcds) + j;
-  const int nqg = (S + QG - 1) / QG;
-  int c = 0, base = 0;
-  for (;;) {
-    const int first = max(g0, c * KC / QG);
-    const int cnt = nqg - first;
-    if (lin < base + cnt) {
-      qg = first + (lin - base);
-      break;
-    }
-    base += cnt;
-    ++c;
+// Work of the block kernel is the sequence of units (query group qg, key
+// tile t) for t < tiles(qg), ordered by group, then tile; tiles(qg) counts
+// the key tiles at or below the group's last query (causal, Section 4.2).
+// The grid is persistent, as many workgroups as fit on the chip at once, and
+// splits the sequence into equal contiguous runs: every CU gets the same
+// number of key tiles (to one) whatever the causal shape, key tiles stream
+// through one pipeline across unit boundaries, and query operands are
+// reloaded only where a run enters a new group. Workgroup i (which the
+// hardware places on XCD i % 8) takes run (i % 8) * n/8 + i / 8 (remainder
+// spread over the first XCDs), so each XCD's L2 sees a contiguous range of
+// groups and the key tiles they share.
+// g0: first query group (a chunked call starting at g0 * QG covers groups
+// g0 ..).
+template <int QG, int KT>
+struct UnitCursor {
+  int S, qg, t, nt;   // sequence length, current group, tile, tiles of the group
+  __host__ __device__ static int tiles(int S, int g) {
+    return (min((g + 1) * QG, S) + KT - 1) / KT;
   }
-  kc = c;
+  __device__ void seek(int g0, long long u) {
+    qg = g0;
+    for (;;) {
+      nt = tiles(S, qg);
+      if (u < nt) break;
+      u -= nt;
+      ++qg;
+    }
+    t = (int)u;
+  }
+};
+
+__device__ __forceinline__ int xcd_run(int i, int n) {
+  const int x = i % kXcds, j = i / kXcds;
+  return x * (n / kXcds) + min(x, n % kXcds) + j;
 }
 
-template <int QG, int KC>
-int count_items(int S, int g0) {
-  const int nqg = (S + QG - 1) / QG, nkc = (S + KC - 1) / KC;
-  int n = 0;
-  for (int c = 0; c < nkc; ++c) n += nqg - max(g0, c * KC / QG);
+template <int QG, int KT>
+long long count_units(int S, int g0) {
+  long long n = 0;
+  for (int g = g0; g * QG < S; ++g) n += UnitCursor<QG, KT>::tiles(S, g);
   return n;
 }
 
-// Key tiles of the block kernel: NSUB sub-tiles of 64 keys, staged
-// PD tiles ahead through registers into a ring of PD + 1 LDS buffers.
+// Key tiles of the block kernel: NSUB sub-tiles of 64 keys, staged one tile
+// ahead through registers into double-buffered LDS.
 template <int DI>
 struct BlockTile {
   static constexpr int NSUB = DI <= 128 ? 2 : 1;
-  static constexpr int PD = 1;
   static constexpr int KT = 64 * NSUB;
   static constexpr int RB = DI * 2 + 16;
   static constexpr int BYTES = KT * RB;
-  static constexpr int NB = PD + 1;
 };
 
 template <int DI, int KT, int RB, int NT>
@@ -164,49 +175,39 @@ __device__ __forceinline__ float half_combine(float x, Op op) {
 // column n for queries 8i + 4h + r. A selection block's aggregate is then a
 // lane-local reduction plus one half-wave combine, and the half index h picks
 // which key tile or block a lane stores, so every store row is contiguous.
-template <int DI, int BQ, bool MAXPOS, int NW, int KC>
-__global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_items, int g0,
+template <int DI, int BQ, bool MAXPOS, int NW>
+__global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, int n_units,
                                                                 int agg, int relu, float scale,
                                                                 const uint16_t *__restrict__ qi,
                                                                 const uint16_t *__restrict__ ki,
                                                                 float *__restrict__ Y) {
   using T = BlockTile<DI>;
   constexpr int NT = NW * 64;
-  constexpr int KT = T::KT, RB = T::RB, KS = DI / 16, NSUB = T::NSUB, PD = T::PD, NB = T::NB;
+  constexpr int KT = T::KT, RB = T::RB, KS = DI / 16, NSUB = T::NSUB;
   constexpr int QG = NW * kQW;
-  static_assert(KC % QG == 0 || QG % KC == 0, "chunk and query group sizes must nest");
-  static_assert(KC % KT == 0, "chunks hold whole tiles");
-  __shared__ __align__(16) char lds[NB][T::BYTES];
+  static_assert(QG % KT == 0, "query groups hold whole key tiles");
+  __shared__ __align__(16) char lds[2][T::BYTES];
   __shared__ float red[NW / 2][KT];
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 31, h = lane >> 5;
-  int qg, kc;
-  decode_item<QG, KC>(blockIdx.x, n_items, S, g0, qg, kc);
-  const int q0 = qg * QG;
-  const int k_begin = kc * KC;
-  const int q_last = min(q0 + QG, S) - 1;
-  const int k_end = min(k_begin + KC, q_last + 1);
-  const int ntiles = (k_end - k_begin + KT - 1) / KT;
-  const int qw0 = q0 + wave * kQW;
-  const int qw_last = min(qw0 + kQW, S) - 1;  // < qw0 when the wave is past the end
+  const int run = xcd_run(blockIdx.x, gridDim.x);
+  const int u0 = (int)((long long)n_units * run / gridDim.x);
+  const int u1 = (int)((long long)n_units * (run + 1) / gridDim.x);
+  if (u0 == u1) return;
+  UnitCursor<QG, KT> uc;
+  uc.S = S;
+  uc.seek(g0, u0);
 
-  // A operands: query tile qt (32 queries), k-step ks: row qw0 + 32qt + n,
-  // dims 16ks + 8h .. + 7
+  // A operands of the current group: query tile qt (32 queries), k-step ks:
+  // row qw0 + 32qt + n, dims 16ks + 8h .. + 7
+  int qw0 = 0, qw_last = -1;   // qw_last < qw0 when the wave is past the end
   bf16x8 a[2][KS];
-#pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
-    const int row = min(qw0 + qt * 32 + n, S - 1);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      a[qt][ks] = as_bf16x8(ldg16(qi + (size_t)row * DI + ks * 16 + h * 8));
-  }
 
-  KeyStageT<DI, KT, RB, NT> stage[PD];
-#pragma unroll
-  for (int j = 0; j < PD; ++j)
-    if (j < ntiles) stage[j].load(ki, S, k_begin + j * KT, tid);
-  stage[0].store(lds[0], tid);
+  KeyStageT<DI, KT, RB, NT> stage;
+  stage.load(ki, S, uc.t * KT, tid);
+  stage.store(lds[0], tid);
   __syncthreads();
 
   const float neutral = agg == SP_AGG_MAX ? -INFINITY : 0.f;
@@ -313,11 +314,7 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_ite
   auto v_key = [&](int v) { return BPW == 1 ? 32 * h + n : 32 * (v / (BPW / 2)) + n; };
   auto v_block = [&](int v) { return BPW == 1 ? 0 : 2 * (v % (BPW / 2)) + h; };
 
-  auto tile = [&](int it, auto j_) {
-    constexpr int j = decltype(j_)::value;   // it % PD
-    const int kt0 = k_begin + it * KT;
-    if (it + PD < ntiles) stage[j].load(ki, S, kt0 + PD * KT, tid);
-    const char *cur = lds[it % NB];
+  auto tile = [&](int kt0, const char *cur) {
     float out[NSUB][NV];
     // (DI = 256 keeps one code path: its 128 query registers leave no room
     // for two instantiations of the sub-tile)
@@ -366,13 +363,30 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int n_ite
         }
       }
     }
-    if (it + 1 < ntiles) stage[(j + 1) % PD].store(lds[(it + 1) % NB], tid);
-    __syncthreads();
   };
-  for (int it0 = 0; it0 < ntiles; it0 += PD) {
-    static_for<0, PD>([&](auto j_) {
-      if (it0 + decltype(j_)::value < ntiles) tile(it0 + decltype(j_)::value, j_);
-    });
+  // groups of the run; the key pipeline runs on across group boundaries
+  for (int u = u0; u < u1;) {
+    const int group = uc.qg, nt = uc.nt;
+    qw0 = group * QG + wave * kQW;
+    qw_last = min(qw0 + kQW, S) - 1;
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      const int row = min(qw0 + qt * 32 + n, S - 1);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        a[qt][ks] = as_bf16x8(ldg16(qi + (size_t)row * DI + ks * 16 + h * 8));
+    }
+    const int t_end = min(nt, uc.t + (u1 - u));
+    for (int t = uc.t; t < t_end; ++t, ++u) {
+      const bool more = u + 1 < u1;
+      if (more) stage.load(ki, S, t + 1 < nt ? (t + 1) * KT : 0, tid);
+      tile(t * KT, lds[(u - u0) & 1]);
+      if (more) stage.store(lds[(u - u0 + 1) & 1], tid);
+      __syncthreads();
+    }
+    uc.qg = group + 1;
+    uc.t = 0;
+    uc.nt = UnitCursor<QG, KT>::tiles(S, group + 1);
   }
 }
 
@@ -461,6 +475,38 @@ __global__ __launch_bounds__(256) void indexer_rows_kernel(int S, int qo, int re
   }
 }
 
+// Launches `kernel` as a persistent grid: as many workgroups as are resident
+// on the current device at once (CUs times the kernel's occupancy, both
+// cached per device), at most one per unit of work.
+template <class... KArgs, class... Args>
+hipError_t launch_persistent(void (*kernel)(KArgs...), int threads, int n_units,
+                             hipStream_t st, Args... args) {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> per_cu{0};
+  static std::atomic<int> cus[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  int c = cus[dev].load(std::memory_order_relaxed);
+  if (c == 0) {
+    e = hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    cus[dev].store(c, std::memory_order_relaxed);
+  }
+  int w = per_cu.load(std::memory_order_relaxed);
+  if (w == 0) {
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&w, kernel, threads, 0);
+    if (e != hipSuccess) return e;
+    w = w < 1 ? 1 : w;
+    per_cu.store(w, std::memory_order_relaxed);
+  }
+  const int grid = n_units < c * w ? n_units : c * w;
+  if (grid == 0) return hipSuccess;
+  hipLaunchKernelGGL(kernel, dim3(grid), dim3(threads), 0, st, args...);
+  return hipGetLastError();
+}
+
 template <int DI>
 hipError_t launch_di(const Prob &p, const void *qi, const void *ki, float *scores,
                      hipStream_t st) {
@@ -479,20 +525,21 @@ hipError_t launch_di(const Prob &p, const void *qi, const void *ki, float *score
                          p.relu, p.iscale, q, k, z);
     return hipGetLastError();
   }
-  constexpr int NW = 8, KC = 1024;
-  const int g0 = p.qo / (NW * kQW);   // a multiple of the query group (checked)
+  constexpr int NW = 8, QG = NW * kQW;
+  const int g0 = p.qo / QG;   // a multiple of the query group (checked)
   float *y = scores - (size_t)(p.qo / p.b) * p.S;
-  const int n_items = count_items<NW * kQW, KC>(p.S, g0);
+  const long long units = count_units<QG, BlockTile<DI>::KT>(p.S, g0);
+  if (units > INT_MAX) return hipErrorInvalidValue;
+  const int n_units = (int)units;
   const bool maxpos = p.agg == SP_AGG_MAX && p.iscale >= 0.f;
 #define SP_BLK(BQ)                                                                           \
   if (maxpos)                                                                                \
-    hipLaunchKernelGGL((indexer_block_kernel<DI, BQ, true, NW, KC>), dim3(n_items),          \
-                       dim3(NW * 64), 0, st, p.S, n_items, g0, p.agg, p.relu, p.iscale, q,   \
-                       k, y);                                                                \
+    err = launch_persistent(indexer_block_kernel<DI, BQ, true, NW>, NW * 64, n_units, st, p.S, \
+                            g0, n_units, p.agg, p.relu, p.iscale, q, k, y);                  \
   else                                                                                       \
-    hipLaunchKernelGGL((indexer_block_kernel<DI, BQ, false, NW, KC>), dim3(n_items),         \
-                       dim3(NW * 64), 0, st, p.S, n_items, g0, p.agg, p.relu, p.iscale, q,   \
-                       k, y)
+    err = launch_persistent(indexer_block_kernel<DI, BQ, false, NW>, NW * 64, n_units, st,   \
+                            p.S, g0, n_units, p.agg, p.relu, p.iscale, q, k, y)
+  hipError_t err;
   switch (p.b) {
     case 16: SP_BLK(16); break;
     case 32: SP_BLK(32); break;
@@ -500,7 +547,7 @@ hipError_t launch_di(const Prob &p, const void *qi, const void *ki, float *score
     default: SP_BLK(128); break;
   }
 #undef SP_BLK
-  return hipGetLastError();
+  return err;
 }
 
 }  // namespace

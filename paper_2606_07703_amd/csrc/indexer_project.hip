@@ -1,5 +1,5 @@
 // Head-collapsed indexer front end on bf16 MFMA (Section 6.3, projection and
-// score equations; Algorithm 2 steps 2-3):
+// score equations; Algorithm 2, indexer projection and its key normalisation, RoPE and query scale):
 //
 //   q_idx[t] = RoPE(W_Q x_t, pos0 + t)
 //   k_idx[t] = RoPE(LN(W_K x_t), pos0 + t),  LN over d_idx with gamma, beta

@@ -1,5 +1,5 @@
 // Fused per-query indexer scoring and top-k selection (Section 6.3 score;
-// Section 6.4 and Algorithm 2 steps 4-5 with b_sel = 1; Section 4.1 TopK):
+// Section 6.4 and Algorithm 2, scoring, selection and sparse prefill with b_sel = 1; Section 4.1 TopK):
 // the top-k of z[t, s] = ReLU(scale <q_idx[t], k_idx[s]>) over s <= t, for
 // every query t, without ever storing the S x S score matrix.
 //

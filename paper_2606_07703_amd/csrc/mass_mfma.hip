@@ -1,5 +1,5 @@
 // Attention-mass oracle scores on bf16 MFMA (Section 4.1 head-averaged mass;
-// Section 4.2 block aggregation; Algorithm 1 step 3):
+// Section 4.2 block aggregation; Algorithm 1, head-averaged probabilities):
 //
 //   P_t(s)    = (1/Hq) sum_h exp(scale <q[t,h], k[s,g(h)]> - lse[t,h]),  s <= t
 //   mass[r,s] = AGG_{t in block r, t >= s} P_t(s)

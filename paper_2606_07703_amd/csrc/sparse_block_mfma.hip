@@ -1,6 +1,6 @@
 // Selection-block-shared sparse GQA attention on bf16 MFMA (Section 3
-// restricted attention; Section 4.2 per-query causal mask; Algorithm 1 step 5
-// and Algorithm 2 step 5: one support per block, replicated over KV heads).
+// restricted attention; Section 4.2 per-query causal mask; Algorithm 1, restricted recomputation
+// and Algorithm 2, selection and sparse GQA prefill: one support per block, replicated over KV heads).
 //
 // One workgroup per (selection block r, KV head j, chunk of up to 256 query
 // rows). A query row is a (query t, head h) pair with g(h) = j; there are

@@ -1,6 +1,6 @@
 // Sparse GQA attention for per-query (or small-block) supports on bf16 MFMA
 // (Section 3 restricted attention; Section 4.2 per-query causal mask;
-// Algorithm 2 step 5 with b_sel = 1).
+// Algorithm 2, selection and sparse GQA prefill with b_sel = 1).
 //
 // Each query owns its support, so there is nothing to share between queries:
 // one wave handles one (query t, KV head j) pair and the G query heads of

@@ -1,11 +1,11 @@
 // Column-parallel support scores with selection-block aggregation, for any
 // shape and dtype (the MFMA kernels cover the large bf16 shapes).
 //
-// Oracle mass (Section 4.1, 4.2; Algorithm 1 step 3):
+// Oracle mass (Section 4.1, 4.2; Algorithm 1, head-averaged probabilities):
 //   P_t(s) = (1/Hq) sum_h exp(scale <q[t,h],k[s,g(h)]> - lse[t,h]),  s <= t
 // or, for the per-KV-group support of the head axis (Section 3), the same
 // average over the G heads of one KV group, one table per group.
-// Indexer score (Section 6.3; Algorithm 2 step 4):
+// Indexer score (Section 6.3; Algorithm 2, candidate scoring):
 //   z[t,s] = ReLU(iscale <q_idx[t], k_idx[s]>),  s <= t
 // Block aggregate (Section 4.2): Y[r,s] = AGG_{t in block r, t >= s} X[t,s].
 //

@@ -1,5 +1,5 @@
 // Top-k support selection per score row (Section 4.1 TopK; Section 4.2;
-// Algorithm 1 steps 4-5; Algorithm 2 step 5).
+// Algorithm 1, selection and restricted recomputation; Algorithm 2, selection and sparse GQA prefill).
 //
 // Row r has L = t1_r+1 causal positions. If L <= k every position is taken.
 // Otherwise the Wf = min(W, k) most recent positions are forced and the

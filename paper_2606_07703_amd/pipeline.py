@@ -1,8 +1,8 @@
 """The three call sequences of the library, with outputs allocated by torch.
 
-* ``indexer_prefill`` — Algorithm 2 steps 4-5: indexer scores, top-k,
+* ``indexer_prefill`` — Algorithm 2, scoring, selection and sparse prefill: indexer scores, top-k,
   sparse GQA attention.
-* ``oracle_prefill`` — Algorithm 1 steps 2-5: dense normalisers, head-averaged
+* ``oracle_prefill`` — Algorithm 1, dense pass, selection and restricted recomputation: dense normalisers, head-averaged
   mass, top-k, sparse GQA attention.
 * ``dense_prefill`` — Section 3 dense causal GQA attention.
 
