@@ -134,36 +134,50 @@ struct TileLoader {
   static constexpr int CHUNKS = (IS_V ? L::VTILE : L::KTILE) / 1024;
   static constexpr int PER = (CHUNKS + NW - 1) / NW;
 
-  // row(e) gives the row of tile entry e (rows outside [0, nrows) read row
-  // 0; their keys are masked). Rows are fetched through a buffer resource
-  // (base and size in SGPRs, 32-bit byte offsets per lane); the API keeps k
-  // and v below 4 GiB.
+  // rows() resolves the row of every chunk this lane loads (row(e) gives the
+  // row of tile entry e; padding slots take entry 0), issue() then fetches
+  // them. Split so that a pipeline can resolve the rows of its next loads
+  // (an LDS lookup for gathered tiles) a step ahead of issuing them.
   template <typename ROW>
-  __device__ __forceinline__ static void load(uint32_t tile, const uint16_t *base, int nrows,
-                                              int Hkv, int j, int wave, int lane, ROW row) {
-    const uint32_t nbytes = (uint32_t)nrows * Hkv * L::RB;
-    const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(base), (short)0,
-                                                      nbytes, kBufferDword3);
-    uint32_t off[PER];
-    bool data[PER];
+  __device__ __forceinline__ static void rows(int wave, int lane, ROW row, int (&out)[PER]) {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int q = wave + p * NW;
       const int slot = (q < CHUNKS ? q : 0) * 64 + lane;
       const int r = slot / SLOTS, c = slot % SLOTS;
-      data[p] = c < L::C;
-      int s = row(data[p] ? r : 0);
-      s = (s >= 0 && s < nrows) ? s : 0;
-      off[p] = ((uint32_t)s * Hkv + j) * L::RB + (data[p] ? c : 0) * 16;
+      out[p] = row(c < L::C ? r : 0);
     }
+  }
+
+  // Rows outside [0, nrows) read row 0; their keys are masked. Rows are
+  // fetched through a buffer resource (base and size in SGPRs, 32-bit byte
+  // offsets per lane); the API keeps k and v below 4 GiB.
+  __device__ __forceinline__ static void issue(uint32_t tile, const uint16_t *base, int nrows,
+                                               int Hkv, int j, int wave, int lane,
+                                               const int (&rw)[PER]) {
+    const uint32_t nbytes = (uint32_t)nrows * Hkv * L::RB;
+    const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(base), (short)0,
+                                                      nbytes, kBufferDword3);
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int q = wave + p * NW;
-      if ((CHUNKS % NW == 0 || q < CHUNKS) && data[p])
+      const int slot = (q < CHUNKS ? q : 0) * 64 + lane;
+      const int c = slot % SLOTS;
+      const int s = (rw[p] >= 0 && rw[p] < nrows) ? rw[p] : 0;
+      const uint32_t off = ((uint32_t)s * Hkv + j) * L::RB + (c < L::C ? c : 0) * 16;
+      if ((CHUNKS % NW == 0 || q < CHUNKS) && c < L::C)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            rs, (__attribute__((address_space(3))) void *)(size_t)(tile + q * 1024), 16, off[p],
+            rs, (__attribute__((address_space(3))) void *)(size_t)(tile + q * 1024), 16, off,
             0, 0, 0);
     }
+  }
+
+  template <typename ROW>
+  __device__ __forceinline__ static void load(uint32_t tile, const uint16_t *base, int nrows,
+                                              int Hkv, int j, int wave, int lane, ROW row) {
+    int rw[PER];
+    rows(wave, lane, row, rw);
+    issue(tile, base, nrows, Hkv, j, wave, lane, rw);
   }
 };
 
@@ -388,18 +402,29 @@ struct AttnPipe {
     return lds + 2 * L::KTILE + (i & 1) * L::VTILE;
   }
 
+  // Rows of the chunks the next load_next issues: K_{n+1} and V_n. A source
+  // whose rows are an LDS lookup (Src::kLookup) resolves them a step ahead;
+  // one whose rows are arithmetic resolves them at issue.
+  using KLoader = TileLoader<D, NW, false>;
+  using VLoader = TileLoader<D, NW, true>;
+  int krows[KLoader::PER], vrows[VLoader::PER];
+  __device__ __forceinline__ void fetch_rows(int n) {
+    if (n + 1 < nt) KLoader::rows(wave, lane, [&](int e) { return src.row(n + 1, e); }, krows);
+    if constexpr (WANT_O)
+      if (n < nt) VLoader::rows(wave, lane, [&](int e) { return src.row(n, e); }, vrows);
+  }
+
   // Tiles of step n + 1: K_{n+1} and V_n, each wave its share of the chunks.
   // Their buffers held K_{n-1} and V_{n-2}, last read in M_{n-1}, before the
-  // barrier that opened step n. Issued at the top of the step: the row
-  // indices are read before the first load.
+  // barrier that opened step n. Issued at the top of the step; for looked-up
+  // rows, from rows resolved one step earlier, and the rows of the next
+  // step's loads are then looked up while this step's phases run.
   __device__ __forceinline__ void load_next(int n) {
-    if (n + 1 < nt)
-      TileLoader<D, NW, false>::load(ktile(n + 1), k, kv_rows, Hkv, j, wave, lane,
-                                     [&](int e) { return src.row(n + 1, e); });
+    if constexpr (!Src::kLookup) fetch_rows(n);
+    if (n + 1 < nt) KLoader::issue(ktile(n + 1), k, kv_rows, Hkv, j, wave, lane, krows);
     if constexpr (WANT_O)
-      if (n < nt)
-        TileLoader<D, NW, true>::load(vtile(n), v, kv_rows, Hkv, j, wave, lane,
-                                      [&](int e) { return src.row(n, e); });
+      if (n < nt) VLoader::issue(vtile(n), v, kv_rows, Hkv, j, wave, lane, vrows);
+    if constexpr (Src::kLookup) fetch_rows(n + 1);
   }
 
   // M_n: QK (n < nt) and PV (n >= 1)
@@ -463,6 +488,7 @@ struct AttnPipe {
     if (nt <= 0) return;
     TileLoader<D, NW, false>::load(ktile(0), k, kv_rows, Hkv, j, wave, lane,
                                    [&](int e) { return src.row(0, e); });
+    if constexpr (Src::kLookup) fetch_rows(0);
     drain_memory();
     __syncthreads();
     // Every step: all waves issue the next step's loads, run their phases

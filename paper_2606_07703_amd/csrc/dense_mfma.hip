@@ -22,6 +22,7 @@ namespace {
 constexpr int kNW = 8;
 
 struct DenseKeys {
+  static constexpr bool kLookup = false;   // rows are arithmetic
   int ntiles, S;
   __device__ __forceinline__ int row(int tile, int e) const { return tile * kAttnKT + e; }
   __device__ __forceinline__ bool needs_mask(int tile, int wave_tmin) const {

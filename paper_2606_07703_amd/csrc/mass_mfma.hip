@@ -4,20 +4,28 @@
 //   P_t(s)    = (1/Hq) sum_h exp(scale <q[t,h], k[s,g(h)]> - lse[t,h]),  s <= t
 //   mass[r,s] = AGG_{t in block r, t >= s} P_t(s)
 //
-// The sum runs over every query head, so one workgroup owns all Hq heads of
-// 16 queries at a time: wave w (of 8) holds the Q fragments of heads
-// w, w+8, ... for those queries in registers. A tile of 32 keys of every KV
-// head (contiguous in memory) is staged in LDS; each wave forms its heads'
-// transposed scores S^T = K Q^T with MFMA, exponentiates against the
-// normaliser and sums over its heads in registers. The eight per-wave partial
-// sums are then added in LDS, masked causally and scaled by 1/Hq.
+// The sum runs over every query head, so a workgroup owns all Hq heads of its
+// queries; each wave holds the query operands of Hq/8 heads in registers and
+// sums its heads in registers, and the eight per-wave partial sums are added
+// in LDS.
 //
-// b = 1: the workgroup covers 16 queries and one chunk of keys and stores
-// P rows directly. b a multiple of 16: the workgroup covers one selection
-// block (b/16 groups of 16 queries, in turn) and one chunk of keys, and keeps
-// the block aggregate of the chunk in LDS until it is stored.
+// mass32_kernel (b = 1, or b a multiple of 32; the heads of a wave share one
+// KV head): a workgroup covers 32 queries (or the b queries of one block, 32
+// at a time) and a chunk of 1024 keys. Scores are formed transposed on
+// v_mfma_f32_32x32x16_bf16, S^T = K Q^T with keys as rows: a lane then holds
+// one query and 16 keys of a 32-key tile, so its normaliser is one register
+// per head and the head sum is lane-local. The 32-key tile of every KV head
+// is loaded straight into LDS (padded rows); the next tile's loads are issued
+// as soon as the current one is in registers and run under the exponentials.
+//
+// mass_kernel (the other shapes): 16 queries per workgroup on
+// v_mfma_f32_16x16x32_bf16, K staged through registers.
+//
+// b = 1 stores P rows directly. b > 1 keeps the block aggregate of the key
+// chunk in LDS until it is stored.
 #include <math.h>
 
+#include "attn_tile.hpp"
 #include "common.hpp"
 #include "kernels.hpp"
 #include "mfma.hpp"
@@ -207,6 +215,239 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const float *ls
   }
 }
 
+
+// ---------------------------------------------------------------- mass32_kernel
+constexpr int kMT = 32;       // keys per tile; queries per query tile
+constexpr int kMKC = 1024;    // keys per workgroup chunk
+constexpr int kRS = 36;       // row stride (floats) of the partial-sum buffer (bank spread)
+constexpr int kMaxHkv = 8;
+
+template <int D>
+struct Mass32 {
+  static constexpr int KRB = D * 2 + 16;     // padded LDS row of one key of one KV head
+  static constexpr int SLOTS = D / 8 + 1;    // 16-byte slots per row (the last is padding)
+  static constexpr int KS = D / 16;          // k-steps of the 32x32x16 product
+  static constexpr int KBYTES = kMaxHkv * kMT * KRB;
+};
+
+// Sum over the eight partials at LDS byte address a, a + kPartBytes, ... in
+// that order. Inline reads: the compiler would otherwise wait for every
+// direct-to-LDS tile load in flight before an LDS read.
+constexpr int kPartBytes = kMT * kRS * 4;
+__device__ __forceinline__ float sum_partials(uint32_t a) {
+  float x[kNW];
+  asm volatile(
+      "ds_read_b32 %0, %8\n\tds_read_b32 %1, %8 offset:%9\n\t"
+      "ds_read_b32 %2, %8 offset:%10\n\tds_read_b32 %3, %8 offset:%11\n\t"
+      "ds_read_b32 %4, %8 offset:%12\n\tds_read_b32 %5, %8 offset:%13\n\t"
+      "ds_read_b32 %6, %8 offset:%14\n\tds_read_b32 %7, %8 offset:%15\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=v"(x[0]), "=v"(x[1]), "=v"(x[2]), "=v"(x[3]), "=v"(x[4]), "=v"(x[5]), "=v"(x[6]),
+        "=v"(x[7])
+      : "v"(a), "i"(kPartBytes), "i"(2 * kPartBytes), "i"(3 * kPartBytes), "i"(4 * kPartBytes),
+        "i"(5 * kPartBytes), "i"(6 * kPartBytes), "i"(7 * kPartBytes)
+      : "memory");
+  float v = 0.f;
+#pragma unroll
+  for (int p = 0; p < kNW; ++p) v += x[p];
+  return v;
+}
+__device__ __forceinline__ float lds_read_f32(uint32_t a) {
+  float x;
+  asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(x) : "v"(a) : "memory");
+  return x;
+}
+__device__ __forceinline__ void lds_write_f32(uint32_t a, float x) {
+  asm volatile("ds_write_b32 %0, %1" : : "v"(a), "v"(x) : "memory");
+}
+
+template <int D, int HPW, bool ROWS>
+__global__ __launch_bounds__(kNW * 64) void mass32_kernel(
+    int S, int Hq, int Hkv, int G, int b, int agg, float scale_log2,
+    const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
+    const float *__restrict__ lse, float *__restrict__ mass) {
+  using T = Mass32<D>;
+  constexpr int KRB = T::KRB, SLOTS = T::SLOTS, KS = T::KS;
+  __shared__ __align__(16) char ktile[T::KBYTES];
+  __shared__ __align__(16) float red[2][kNW][kMT][kRS];
+  __shared__ float yagg[ROWS ? 1 : kMKC];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 31, half = lane >> 5;
+  const int span = ROWS ? kMT : b;
+  const int tq0 = blockIdx.x * span;
+  const int tq_last = min(tq0 + span, S) - 1;
+  const int k_begin = blockIdx.y * kMKC;
+  if (k_begin > tq_last) return;   // the whole workgroup
+  const int k_end = min(k_begin + kMKC, tq_last + 1);
+  const int h0 = wave * HPW;       // the wave's heads h0 .. h0 + HPW - 1
+  const int jj = h0 / G;           // their KV head
+  const float neutral = agg == SP_AGG_MAX ? -INFINITY : 0.f;
+  const float invH = 1.f / (float)Hq;
+  auto op = [agg](float x, float y) { return agg == SP_AGG_MAX ? fmaxf(x, y) : x + y; };
+  if constexpr (!ROWS)
+    for (int i = tid; i < kMKC; i += kNW * 64) yagg[i] = neutral;
+
+  // K tile: row jj * 32 + key, slot c of a row at byte (row * SLOTS + c) * 16,
+  // so chunk c of 64 slots is 1 KiB at c * 1024; lanes on padding slots and
+  // past the last row load nothing. Keys past S - 1 read row S - 1 (masked).
+  const int rows = Hkv * kMT, chunks = (rows * SLOTS + 63) / 64;
+  const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(k), (short)0,
+                                                    (uint32_t)S * Hkv * D * 2, kBufferDword3);
+  const uint32_t kt = (uint32_t)(size_t)(__attribute__((address_space(3))) char *)ktile;
+  auto issue_k = [&](int k0) {
+    for (int c = wave; c < chunks; c += kNW) {
+      const int slot = c * 64 + lane;
+      const int row = slot / SLOTS, col = slot % SLOTS;
+      if (row < rows && col < SLOTS - 1) {
+        const int s = min(k0 + row % kMT, S - 1);
+        const uint32_t off = (((uint32_t)s * Hkv + row / kMT) * D + col * 8) * 2;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rs, (__attribute__((address_space(3))) void *)(size_t)(kt + c * 1024), 16, off, 0,
+            0, 0);
+      }
+    }
+  };
+
+  // B operands of the wave's heads for query tqt + n: dims 16 ks + 8 half ..
+  bf16x8 qf[HPW][KS];
+  float lse2[HPW];
+  auto load_q = [&](int tqt) {
+    const int t = min(tqt + n, S - 1);
+#pragma unroll
+    for (int hh = 0; hh < HPW; ++hh) {
+      const uint16_t *qp = q + ((size_t)t * Hq + h0 + hh) * D + half * 8;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) qf[hh][ks] = as_bf16x8(ldg16(qp + ks * 16));
+      lse2[hh] = lse[(size_t)t * Hq + h0 + hh] * kLog2e;
+    }
+  };
+
+  // Sum of the eight partials of tile (buffer rb, keys k0 .., queries tqt ..)
+  // in wave order, scaled by 1/Hq; masked causally. b = 1: lane -> key
+  // lane % 32, rows 4 wave + 2 half + e, stored. b > 1: lane -> key
+  // (64 wave + lane) / 16, rows 2 (lane % 16) + e; the block aggregate over
+  // the tile's rows goes into yagg.
+  const uint32_t red_a = (uint32_t)(size_t)(__attribute__((address_space(3))) float *)&red[0][0][0][0];
+  const uint32_t yagg_a = (uint32_t)(size_t)(__attribute__((address_space(3))) float *)yagg;
+  auto reduce = [&](int rb, int k0, int tqt) {
+    const uint32_t base = red_a + rb * (kNW * kPartBytes);
+    if constexpr (ROWS) {
+      const int kk = lane & 31, s = k0 + kk;
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int row = 4 * wave + 2 * half + e, t = tqt + row;
+        const float v = sum_partials(base + (row * kRS + kk) * 4);
+        if (t <= tq_last && s <= t) mass[(size_t)t * S + s] = v * invH;
+      }
+    } else {
+      const int kk = (wave * 64 + lane) >> 4, r2 = lane & 15, s = k0 + kk;
+      float x = neutral;
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int row = 2 * r2 + e, t = tqt + row;
+        const float v = sum_partials(base + (row * kRS + kk) * 4);
+        if (t <= tq_last && s <= t) x = op(x, v * invH);
+      }
+#pragma unroll
+      for (int off = 8; off > 0; off >>= 1) x = op(x, __shfl_xor(x, off, 16));
+      if (r2 == 0 && s < k_end) {
+        const uint32_t ya = yagg_a + (s - k_begin) * 4;
+        lds_write_f32(ya, op(lds_read_f32(ya), x));
+      }
+    }
+  };
+
+  const char *krow = ktile + (jj * kMT + n) * KRB + half * 16;
+  int rb = 0;
+  for (int tqt = tq0; tqt <= tq_last; tqt += kMT) {   // query tiles (one when b = 1)
+    const int t_hi = min(tqt + kMT, S) - 1;
+    const int ke = min(k_end, t_hi + 1);
+    if (k_begin >= ke) continue;   // uniform
+    const int ntiles = (ke - k_begin + kMT - 1) / kMT;
+    load_q(tqt);
+    __syncthreads();   // the previous query tile's K tile and partials are consumed
+    issue_k(k_begin);
+    for (int it = 0; it < ntiles; ++it) {
+      const int k0 = k_begin + it * kMT;
+      wait_loads<0>();
+      __syncthreads();   // K tile it in LDS
+      bf16x8 kf[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kf[ks] = as_bf16x8(lds16(krow + ks * 32));
+      __syncthreads();   // every wave holds its K operands: the buffer is free
+      if (it + 1 < ntiles) issue_k(k0 + kMT);
+      // rows of the previous key tile (their stores complete under this tile)
+      if (it > 0) reduce(rb ^ 1, k0 - kMT, tqt);
+      f32x16 psum;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) psum[e] = 0.f;
+#pragma unroll
+      for (int hh = 0; hh < HPW; ++hh) {
+        f32x16 acc;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) acc = mfma32(kf[ks], qf[hh][ks], acc);
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          psum[e] += __builtin_amdgcn_exp2f(fmaf(acc[e], scale_log2, -lse2[hh]));
+      }
+      // lane (n, half) holds query n, keys 8i + 4 half + r: element 4i + r
+      float *rw = &red[rb][wave][n][half * 4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<float4 *>(rw + 8 * i) =
+            make_float4(psum[4 * i], psum[4 * i + 1], psum[4 * i + 2], psum[4 * i + 3]);
+      __syncthreads();   // partials of tile it complete
+      rb ^= 1;
+    }
+    reduce(rb ^ 1, k_begin + (ntiles - 1) * kMT, tqt);
+  }
+  if constexpr (!ROWS) {
+    __syncthreads();
+    for (int i = tid; i < k_end - k_begin; i += kNW * 64)
+      mass[(size_t)blockIdx.x * S + k_begin + i] = yagg[i];
+  }
+}
+
+template <int D, int HPW>
+hipError_t launch32_t(const Prob &p, const void *q, const void *k, const float *lse,
+                      float *mass, hipStream_t st) {
+  const bool rows = p.b == 1;
+  const int span = rows ? kMT : p.b;
+  dim3 grid((p.S + span - 1) / span, (p.S + kMKC - 1) / kMKC);
+  if (rows)
+    hipLaunchKernelGGL((mass32_kernel<D, HPW, true>), grid, dim3(kNW * 64), 0, st, p.S, p.Hq,
+                       p.Hkv, p.G, p.b, p.agg, p.scale * kLog2e, (const uint16_t *)q,
+                       (const uint16_t *)k, lse, mass);
+  else
+    hipLaunchKernelGGL((mass32_kernel<D, HPW, false>), grid, dim3(kNW * 64), 0, st, p.S, p.Hq,
+                       p.Hkv, p.G, p.b, p.agg, p.scale * kLog2e, (const uint16_t *)q,
+                       (const uint16_t *)k, lse, mass);
+  return hipGetLastError();
+}
+
+bool mass32_supported(const Prob &p) {
+  const int hpw = p.Hq / kNW;
+  return p.Hq % kNW == 0 && (hpw == 1 || hpw == 2 || hpw == 4 || (hpw == 8 && p.d == 64)) &&
+         p.G % hpw == 0 && p.Hkv <= kMaxHkv && (p.b == 1 || p.b % kMT == 0);
+}
+
+template <int D>
+hipError_t launch32_d(const Prob &p, const void *q, const void *k, const float *lse,
+                      float *mass, hipStream_t st) {
+  switch (p.Hq / kNW) {
+    case 1: return launch32_t<D, 1>(p, q, k, lse, mass, st);
+    case 2: return launch32_t<D, 2>(p, q, k, lse, mass, st);
+    case 4: return launch32_t<D, 4>(p, q, k, lse, mass, st);
+    default:
+      if constexpr (D == 64) return launch32_t<D, 8>(p, q, k, lse, mass, st);
+      return hipErrorInvalidValue;
+  }
+}
+
 }  // namespace
 
 bool mass_mfma_supported(const Prob &p) {
@@ -219,6 +460,10 @@ bool mass_mfma_supported(const Prob &p) {
 
 hipError_t launch_mass_mfma(const Prob &p, const void *q, const void *k, const float *lse,
                             float *mass, hipStream_t st) {
+  if (mass32_supported(p)) {
+    if (p.d == 64) return launch32_d<64>(p, q, k, lse, mass, st);
+    return launch32_d<128>(p, q, k, lse, mass, st);
+  }
   if (p.d == 64) return launch_d<64>(p, q, k, lse, mass, st);
   return launch_d<128>(p, q, k, lse, mass, st);
 }

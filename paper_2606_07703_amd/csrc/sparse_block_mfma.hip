@@ -31,6 +31,7 @@ constexpr int kMaxTiles = kMaxSupport / kAttnKT;
 // for this wave (a bit per tile, kept in registers so the softmax phase reads
 // no LDS).
 struct SupportKeys {
+  static constexpr bool kLookup = true;   // rows are read from the LDS support cache
   int ntiles;
   const int *pos;
   const int *rows;
