@@ -230,27 +230,37 @@ struct Mass32 {
   static constexpr int KBYTES = kMaxHkv * kMT * KRB;
 };
 
-// Sum over the eight partials at LDS byte address a, a + kPartBytes, ... in
-// that order. Inline reads: the compiler would otherwise wait for every
-// direct-to-LDS tile load in flight before an LDS read.
 constexpr int kPartBytes = kMT * kRS * 4;
-__device__ __forceinline__ float sum_partials(uint32_t a) {
-  float x[kNW];
+// Sums over the eight partials at LDS byte addresses a0, a0 + kPartBytes, ...
+// and a1, a1 + kPartBytes, ..., each in that order, with one wait. Inline
+// reads: the compiler would otherwise wait for every direct-to-LDS tile load
+// in flight before an LDS read. The outputs are early-clobber: a read's data
+// may land while later reads of the block still need the address registers.
+__device__ __forceinline__ void sum_partials2(uint32_t a0, uint32_t a1, float &v0, float &v1) {
+  float x[kNW], y[kNW];
   asm volatile(
-      "ds_read_b32 %0, %8\n\tds_read_b32 %1, %8 offset:%9\n\t"
-      "ds_read_b32 %2, %8 offset:%10\n\tds_read_b32 %3, %8 offset:%11\n\t"
-      "ds_read_b32 %4, %8 offset:%12\n\tds_read_b32 %5, %8 offset:%13\n\t"
-      "ds_read_b32 %6, %8 offset:%14\n\tds_read_b32 %7, %8 offset:%15\n\t"
+      "ds_read_b32 %0, %16\n\tds_read_b32 %1, %16 offset:%18\n\t"
+      "ds_read_b32 %2, %16 offset:%19\n\tds_read_b32 %3, %16 offset:%20\n\t"
+      "ds_read_b32 %4, %16 offset:%21\n\tds_read_b32 %5, %16 offset:%22\n\t"
+      "ds_read_b32 %6, %16 offset:%23\n\tds_read_b32 %7, %16 offset:%24\n\t"
+      "ds_read_b32 %8, %17\n\tds_read_b32 %9, %17 offset:%18\n\t"
+      "ds_read_b32 %10, %17 offset:%19\n\tds_read_b32 %11, %17 offset:%20\n\t"
+      "ds_read_b32 %12, %17 offset:%21\n\tds_read_b32 %13, %17 offset:%22\n\t"
+      "ds_read_b32 %14, %17 offset:%23\n\tds_read_b32 %15, %17 offset:%24\n\t"
       "s_waitcnt lgkmcnt(0)"
-      : "=v"(x[0]), "=v"(x[1]), "=v"(x[2]), "=v"(x[3]), "=v"(x[4]), "=v"(x[5]), "=v"(x[6]),
-        "=v"(x[7])
-      : "v"(a), "i"(kPartBytes), "i"(2 * kPartBytes), "i"(3 * kPartBytes), "i"(4 * kPartBytes),
-        "i"(5 * kPartBytes), "i"(6 * kPartBytes), "i"(7 * kPartBytes)
+      : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3]), "=&v"(x[4]), "=&v"(x[5]),
+        "=&v"(x[6]), "=&v"(x[7]), "=&v"(y[0]), "=&v"(y[1]), "=&v"(y[2]), "=&v"(y[3]),
+        "=&v"(y[4]), "=&v"(y[5]), "=&v"(y[6]), "=&v"(y[7])
+      : "v"(a0), "v"(a1), "i"(kPartBytes), "i"(2 * kPartBytes), "i"(3 * kPartBytes),
+        "i"(4 * kPartBytes), "i"(5 * kPartBytes), "i"(6 * kPartBytes), "i"(7 * kPartBytes)
       : "memory");
-  float v = 0.f;
+  v0 = 0.f;
+  v1 = 0.f;
 #pragma unroll
-  for (int p = 0; p < kNW; ++p) v += x[p];
-  return v;
+  for (int p = 0; p < kNW; ++p) {
+    v0 += x[p];
+    v1 += y[p];
+  }
 }
 __device__ __forceinline__ float lds_read_f32(uint32_t a) {
   float x;
@@ -290,23 +300,43 @@ __global__ __launch_bounds__(kNW * 64) void mass32_kernel(
     for (int i = tid; i < kMKC; i += kNW * 64) yagg[i] = neutral;
 
   // K tile: row jj * 32 + key, slot c of a row at byte (row * SLOTS + c) * 16,
-  // so chunk c of 64 slots is 1 KiB at c * 1024; lanes on padding slots and
-  // past the last row load nothing. Keys past S - 1 read row S - 1 (masked).
+  // so chunk c of 64 slots is 1 KiB at c * 1024. A lane's byte offset within
+  // a tile of keys k0 .. is fixed (kept in registers, ~0 for lanes on padding
+  // slots or past the last row, which load nothing). Keys past S - 1 fall
+  // outside the buffer and load zeros (they are masked).
+  constexpr int kMaxChunks = (kMaxHkv * kMT * SLOTS + 63) / 64;
+  constexpr int kCPW = (kMaxChunks + kNW - 1) / kNW;   // chunks per wave, at most
   const int rows = Hkv * kMT, chunks = (rows * SLOTS + 63) / 64;
+  const uint32_t key_bytes = (uint32_t)Hkv * D * 2;
   const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(k), (short)0,
-                                                    (uint32_t)S * Hkv * D * 2, kBufferDword3);
+                                                    (uint32_t)S * key_bytes, kBufferDword3);
   const uint32_t kt = (uint32_t)(size_t)(__attribute__((address_space(3))) char *)ktile;
+  auto lane_offset = [&](int i) {
+    const int slot = (wave + i * kNW) * 64 + lane;
+    const int row = slot / SLOTS, col = slot % SLOTS;
+    return (row < rows && col < SLOTS - 1)
+               ? (uint32_t)(row % kMT) * key_bytes + (uint32_t)((row / kMT) * D + col * 8) * 2
+               : ~0u;
+  };
+  // per-query rows keep the offsets in registers; block aggregation (more
+  // live state) recomputes them per tile
+  uint32_t koff[ROWS ? kCPW : 1];
+  if constexpr (ROWS) {
+#pragma unroll
+    for (int i = 0; i < kCPW; ++i) koff[i] = lane_offset(i);
+  }
   auto issue_k = [&](int k0) {
-    for (int c = wave; c < chunks; c += kNW) {
-      const int slot = c * 64 + lane;
-      const int row = slot / SLOTS, col = slot % SLOTS;
-      if (row < rows && col < SLOTS - 1) {
-        const int s = min(k0 + row % kMT, S - 1);
-        const uint32_t off = (((uint32_t)s * Hkv + row / kMT) * D + col * 8) * 2;
+    const uint32_t sb = (uint32_t)k0 * key_bytes;
+#pragma unroll
+    for (int i = 0; i < kCPW; ++i) {
+      const int c = wave + i * kNW;
+      uint32_t off;
+      if constexpr (ROWS) off = koff[i];
+      else off = lane_offset(i);
+      if (c < chunks && off != ~0u)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            rs, (__attribute__((address_space(3))) void *)(size_t)(kt + c * 1024), 16, off, 0,
-            0, 0);
-      }
+            rs, (__attribute__((address_space(3))) void *)(size_t)(kt + c * 1024), 16, off + sb,
+            0, 0, 0);
     }
   };
 
@@ -334,21 +364,23 @@ __global__ __launch_bounds__(kNW * 64) void mass32_kernel(
   auto reduce = [&](int rb, int k0, int tqt) {
     const uint32_t base = red_a + rb * (kNW * kPartBytes);
     if constexpr (ROWS) {
-      const int kk = lane & 31, s = k0 + kk;
+      const int kk = lane & 31, s = k0 + kk, row = 4 * wave + 2 * half;
+      float v[2];
+      sum_partials2(base + (row * kRS + kk) * 4, base + ((row + 1) * kRS + kk) * 4, v[0], v[1]);
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        const int row = 4 * wave + 2 * half + e, t = tqt + row;
-        const float v = sum_partials(base + (row * kRS + kk) * 4);
-        if (t <= tq_last && s <= t) mass[(size_t)t * S + s] = v * invH;
+        const int t = tqt + row + e;
+        if (t <= tq_last && s <= t) mass[(size_t)t * S + s] = v[e] * invH;
       }
     } else {
-      const int kk = (wave * 64 + lane) >> 4, r2 = lane & 15, s = k0 + kk;
+      const int kk = (wave * 64 + lane) >> 4, r2 = lane & 15, s = k0 + kk, row = 2 * r2;
+      float v[2];
+      sum_partials2(base + (row * kRS + kk) * 4, base + ((row + 1) * kRS + kk) * 4, v[0], v[1]);
       float x = neutral;
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        const int row = 2 * r2 + e, t = tqt + row;
-        const float v = sum_partials(base + (row * kRS + kk) * 4);
-        if (t <= tq_last && s <= t) x = op(x, v * invH);
+        const int t = tqt + row + e;
+        if (t <= tq_last && s <= t) x = op(x, v[e] * invH);
       }
 #pragma unroll
       for (int off = 8; off > 0; off >>= 1) x = op(x, __shfl_xor(x, off, 16));
@@ -380,29 +412,47 @@ __global__ __launch_bounds__(kNW * 64) void mass32_kernel(
       if (it + 1 < ntiles) issue_k(k0 + kMT);
       // rows of the previous key tile (their stores complete under this tile)
       if (it > 0) reduce(rb ^ 1, k0 - kMT, tqt);
+      // Heads are pipelined: the products of head hh + 1 issue between the
+      // exponentials of head hh (one MFMA, then its share of the vector work),
+      // so the matrix core runs while the wave exponentiates.
       f32x16 psum;
 #pragma unroll
       for (int e = 0; e < 16; ++e) psum[e] = 0.f;
+      f32x16 acc[2];
+      auto products = [&](int hh, f32x16 &c) {
 #pragma unroll
-      for (int hh = 0; hh < HPW; ++hh) {
-        f32x16 acc;
+        for (int e = 0; e < 16; ++e) c[e] = 0.f;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) acc = mfma32(kf[ks], qf[hh][ks], acc);
+        for (int ks = 0; ks < KS; ++ks) c = mfma32(kf[ks], qf[hh][ks], c);
+      };
+      auto exponentials = [&](int hh, const f32x16 &c) {
 #pragma unroll
         for (int e = 0; e < 16; ++e)
-          psum[e] += __builtin_amdgcn_exp2f(fmaf(acc[e], scale_log2, -lse2[hh]));
+          psum[e] += __builtin_amdgcn_exp2f(fmaf(c[e], scale_log2, -lse2[hh]));
+      };
+      products(0, acc[0]);
+#pragma unroll
+      for (int hh = 1; hh < HPW; ++hh) {
+        products(hh, acc[hh & 1]);
+        exponentials(hh - 1, acc[(hh - 1) & 1]);
+        // 48 vector instructions over the KS products: one MFMA, then 48 / KS
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 48 / KS, 0);
+        }
       }
+      exponentials(HPW - 1, acc[(HPW - 1) & 1]);
       // lane (n, half) holds query n, keys 8i + 4 half + r: element 4i + r
       float *rw = &red[rb][wave][n][half * 4];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         *reinterpret_cast<float4 *>(rw + 8 * i) =
             make_float4(psum[4 * i], psum[4 * i + 1], psum[4 * i + 2], psum[4 * i + 3]);
-      __syncthreads();   // partials of tile it complete
+      // the next tile's first barrier publishes these partials to its reduce
       rb ^= 1;
     }
+    __syncthreads();   // partials of the last tile complete
     reduce(rb ^ 1, k_begin + (ntiles - 1) * kMT, tqt);
   }
   if constexpr (!ROWS) {
