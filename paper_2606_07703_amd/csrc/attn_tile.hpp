@@ -149,23 +149,25 @@ struct TileLoader {
     }
   }
 
-  // Rows outside [0, nrows) read row 0; their keys are masked. Rows are
-  // fetched through a buffer resource (base and size in SGPRs, 32-bit byte
-  // offsets per lane); the API keeps k and v below 4 GiB.
+  // Rows outside [0, nrows) read row 0; their keys are masked. Lanes on
+  // padding slots load the row's first 16 bytes into their padding slot,
+  // which nothing reads: no lane of a chunk is masked. Rows are fetched
+  // through a buffer resource (base and size in SGPRs, 32-bit byte offsets
+  // per lane); the API keeps k and v below 4 GiB.
   __device__ __forceinline__ static void issue(uint32_t tile, const uint16_t *base, int nrows,
                                                int Hkv, int j, int wave, int lane,
                                                const int (&rw)[PER]) {
-    const uint32_t nbytes = (uint32_t)nrows * Hkv * L::RB;
+    const uint32_t row_bytes = (uint32_t)Hkv * L::RB;
     const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(base), (short)0,
-                                                      nbytes, kBufferDword3);
+                                                      (uint32_t)nrows * row_bytes, kBufferDword3);
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int q = wave + p * NW;
       const int slot = (q < CHUNKS ? q : 0) * 64 + lane;
       const int c = slot % SLOTS;
-      const int s = (rw[p] >= 0 && rw[p] < nrows) ? rw[p] : 0;
-      const uint32_t off = ((uint32_t)s * Hkv + j) * L::RB + (c < L::C ? c : 0) * 16;
-      if ((CHUNKS % NW == 0 || q < CHUNKS) && c < L::C)
+      const uint32_t s = (rw[p] >= 0 && rw[p] < nrows) ? (uint32_t)rw[p] : 0u;
+      const uint32_t off = s * row_bytes + (uint32_t)(j * L::RB + (c < L::C ? c : 0) * 16);
+      if (CHUNKS % NW == 0 || q < CHUNKS)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
             rs, (__attribute__((address_space(3))) void *)(size_t)(tile + q * 1024), 16, off,
             0, 0, 0);
