@@ -418,14 +418,18 @@ struct AttnPipe {
 
   // Tiles of step n + 1: K_{n+1} and V_n, each wave its share of the chunks.
   // Their buffers held K_{n-1} and V_{n-2}, last read in M_{n-1}, before the
-  // barrier that opened step n. Issued at the top of the step; for looked-up
-  // rows, from rows resolved one step earlier, and the rows of the next
-  // step's loads are then looked up while this step's phases run.
+  // barrier that opened step n. Issued at the top of the step; looked-up rows
+  // were resolved during the previous step (lookup_next).
   __device__ __forceinline__ void load_next(int n) {
     if constexpr (!Src::kLookup) fetch_rows(n);
     if (n + 1 < nt) KLoader::issue(ktile(n + 1), k, kv_rows, Hkv, j, wave, lane, krows);
     if constexpr (WANT_O)
       if (n < nt) VLoader::issue(vtile(n), v, kv_rows, Hkv, j, wave, lane, vrows);
+  }
+  // Looks up the rows of step n + 1's loads. Called just before a barrier:
+  // the barrier's wait for LDS reads then falls in time the wave would spend
+  // waiting there anyway, not at the start of an MFMA phase.
+  __device__ __forceinline__ void lookup_next(int n) {
     if constexpr (Src::kLookup) fetch_rows(n + 1);
   }
 
@@ -502,18 +506,21 @@ struct AttnPipe {
       load_next(0);
       phase_m<true, false>(0);
       phase_v(0);
+      lookup_next(0);
       end_step();
 #pragma unroll 1
       for (int n = 1; n < nt; ++n) {
         load_next(n);
         phase_m<true, true>(n);
         phase_v(n);
+        lookup_next(n);
         end_step();
       }
       phase_m<false, true>(nt);
     } else if (group == 0) {
       load_next(0);
       phase_m<true, false>(0);
+      lookup_next(0);
       __syncthreads();
       phase_v(0);
       end_step();
@@ -521,6 +528,7 @@ struct AttnPipe {
       for (int n = 1; n < nt; ++n) {
         load_next(n);
         phase_m<true, true>(n);
+        lookup_next(n);
         __syncthreads();
         phase_v(n);
         end_step();
@@ -530,6 +538,7 @@ struct AttnPipe {
       __syncthreads();
     } else {
       load_next(0);
+      lookup_next(0);
       __syncthreads();
       phase_m<true, false>(0);
       end_step();
@@ -537,6 +546,7 @@ struct AttnPipe {
       for (int n = 1; n < nt; ++n) {
         load_next(n);
         phase_v(n - 1);
+        lookup_next(n);
         __syncthreads();
         phase_m<true, true>(n);
         end_step();
