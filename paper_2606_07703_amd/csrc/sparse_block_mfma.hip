@@ -83,16 +83,27 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel
   // Positions in a row are distinct, so at most t1 + 1 entries remain. Each
   // thread takes kEPT consecutive entries per pass (one pass when kk <= 8 NT):
   // all its loads are in flight together, a wave scan of the per-thread
-  // counts gives the write offsets, and one barrier per pass publishes the
-  // wave totals (double-buffered, so passes need no second barrier).
+  // counts (bit-sliced ballots: no LDS round trips) gives the write offsets,
+  // and one barrier per pass publishes the wave totals (double-buffered, so
+  // passes need no second barrier). Each tile's largest position (tkey; the
+  // tile needs the causal mask for queries below it) is raised with LDS
+  // atomics as the entries are written.
   constexpr int kEPT = 8;
+  for (int i = tid; i < kMaxTiles; i += NT) tkey[i] = INT_MIN;
   int nv = 0;
   for (int c0 = 0, pass = 0; c0 < kk; c0 += NT * kEPT, ++pass) {
     const int cb = c0 + tid * kEPT;
     const int32_t *row = idx + (size_t)j * gstride + (size_t)r * kk;
     int sv[kEPT], pr[kEPT];
+    if (cb + kEPT <= kk && (((uintptr_t)(row + cb)) & 15) == 0) {
+      const int4 a = *reinterpret_cast<const int4 *>(row + cb);
+      const int4 c = *reinterpret_cast<const int4 *>(row + cb + 4);
+      sv[0] = a.x; sv[1] = a.y; sv[2] = a.z; sv[3] = a.w;
+      sv[4] = c.x; sv[5] = c.y; sv[6] = c.z; sv[7] = c.w;
+    } else {
 #pragma unroll
-    for (int e = 0; e < kEPT; ++e) sv[e] = cb + e < kk ? row[cb + e] : -1;
+      for (int e = 0; e < kEPT; ++e) sv[e] = cb + e < kk ? row[cb + e] : -1;
+    }
     int cnt = 0;
 #pragma unroll
     for (int e = 0; e < kEPT; ++e) {
@@ -100,15 +111,19 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel
       if constexpr (PAGED) pr[e] = (sv[e] >= 0 && sv[e] <= t1) ? pages.row(sv[e]) : -1;
       cnt += (sv[e] >= 0 && sv[e] <= t1 && pr[e] >= 0);
     }
-    int incl = cnt;   // inclusive scan over the lanes of the wave
+    // exclusive prefix of cnt (0 .. 8, four bits) over the wave, and its total
+    int excl = 0, wtot = 0;
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int y = __shfl_up(incl, off, 64);
-      if (lane >= off) incl += y;
+    for (int bit = 0; bit < 4; ++bit) {
+      const uint64_t m = __ballot((cnt >> bit) & 1);
+      const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+          (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      excl += (int)below << bit;
+      wtot += __popcll(m) << bit;
     }
-    if (lane == 63) red_cnt[pass & 1][wave] = incl;
+    if (lane == 0) red_cnt[pass & 1][wave] = wtot;
     __syncthreads();
-    int pos = nv + incl - cnt;
+    int pos = nv + excl;
     for (int w = 0; w < NW; ++w) {
       const int tw = red_cnt[pass & 1][w];
       if (w < wave) pos += tw;
@@ -119,6 +134,7 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel
       if (sv[e] >= 0 && sv[e] <= t1 && pr[e] >= 0) {
         ir[pos] = sv[e];
         if constexpr (PAGED) irp[pos] = pr[e];
+        atomicMax(&tkey[pos / kAttnKT], sv[e]);
         ++pos;
       }
   }
@@ -127,15 +143,8 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel
     ir[c] = -1;
     if constexpr (PAGED) irp[c] = -1;
   }
-  __syncthreads();
-  // per tile: its largest position, or INT_MAX when it holds padding
-  for (int tile = wave; tile < ntiles; tile += NW) {
-    const int s = ir[tile * kAttnKT + lane];
-    int key = s >= 0 ? s : INT_MAX;
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) key = max(key, __shfl_xor(key, off, 64));
-    if (lane == 0) tkey[tile] = key;
-  }
+  // a tile that holds padding is masked for every query
+  if (tid == 0 && ntiles * kAttnKT > nv) atomicMax(&tkey[ntiles - 1], INT_MAX);
   __syncthreads();
 
   AttnState<D> st;
