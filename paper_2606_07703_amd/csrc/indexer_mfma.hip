@@ -314,18 +314,94 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
   auto v_key = [&](int v) { return BPW == 1 ? 32 * h + n : 32 * (v / (BPW / 2)) + n; };
   auto v_block = [&](int v) { return BPW == 1 ? 0 : 2 * (v % (BPW / 2)) + h; };
 
+  // Tile wholly below the wave's first query (no masks): its 2 NSUB chains of
+  // 32 keys (sub-tile sb, key tile ct) form one stream of operand reads and
+  // products, and the reduction of each chain runs interleaved with the
+  // products of the next, one (query tile, row group) step per operand read,
+  // so the vector work issues while the matrix core runs. Only the last
+  // chain's reduction follows the products.
+  auto full_tile = [&](const char *cur, float (&out)[NSUB][NV]) {
+    constexpr int NCH = 2 * NSUB, NR = NCH * KS, PF = 2, NBF = PF + 1, STEPS = 8;
+    f32x16 acc[2][2];
+    float vals[2][BPW];
+    bf16x8 kb[NBF];
+    const uint32_t kbase =
+        (uint32_t)(size_t)(const __attribute__((address_space(3))) char *)(cur + n * RB + h * 16);
+    // step st of chain pc's reduction: query tile st / 4, row group st % 4
+    auto red_step = [&](auto pc_, auto st_) {
+      constexpr int pc = decltype(pc_)::value, st = decltype(st_)::value;
+      constexpr int c = pc & 1, qt = st >> 2, i = st & 3;
+      if constexpr (st == 0) {
+#pragma unroll
+        for (int bb = 0; bb < BPW; ++bb) vals[c][bb] = neutral;
+      }
+      float x[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        x[r] = acc[c][qt][4 * i + r];
+        if constexpr (!MAXPOS) {
+          x[r] *= scale;
+          if (relu) x[r] = fmaxf(x[r], 0.f);
+        }
+      }
+      constexpr int bb = BPW == 1 ? 0 : (qt * 32 + i * 8) / BQ;
+      vals[c][bb] = op(vals[c][bb], op(op(x[0], x[1]), op(x[2], x[3])));
+    };
+    // chain pc done: combine the half-waves and keep this lane's values
+    auto finalize = [&](auto pc_) {
+      constexpr int pc = decltype(pc_)::value, c = pc & 1, sb = pc >> 1, ct = pc & 1;
+#pragma unroll
+      for (int bb = 0; bb < BPW; ++bb) {
+        float m = half_combine(vals[c][bb], op);
+        if constexpr (MAXPOS) {
+          m *= scale;
+          if (relu) m = fmaxf(m, 0.f);
+        }
+        vals[c][bb] = m;
+      }
+      if constexpr (BPW == 1) {
+        if constexpr (ct == 0) out[sb][0] = vals[c][0];
+        else out[sb][0] = h ? vals[c][0] : out[sb][0];
+      } else {
+#pragma unroll
+        for (int m = 0; m < BPW / 2; ++m)
+          out[sb][ct * (BPW / 2) + m] = h ? vals[c][2 * m + 1] : vals[c][2 * m];
+      }
+    };
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    static_for<0, NR + PF>([&](auto I) {
+      constexpr int x = decltype(I)::value;
+      if constexpr (x < NR) {   // issue read x: chain x / KS, k-step x % KS
+        constexpr int ch = x / KS, ks = x % KS;
+        constexpr int off = (ch >> 1) * 64 * RB + (ch & 1) * 32 * RB + ks * 32;
+        asm volatile("ds_read_b128 %0, %1 offset:%2"
+                     : "=v"(kb[x % NBF])
+                     : "v"(kbase), "i"(off));
+      }
+      if constexpr (x >= PF) {   // products of read x - PF, then reduction steps of the previous chain
+        constexpr int y = x - PF, ch = y / KS, ks = y % KS, c = ch & 1;
+        constexpr int later = (NR - 1 - y < PF ? NR - 1 - y : PF);
+        asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(kb[y % NBF]) : "i"(later));
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt)
+          acc[c][qt] = mfma32(a[qt][ks], kb[y % NBF], ks == 0 ? f32x16{} : acc[c][qt]);
+        if constexpr (ch >= 1) {
+          static_for<ks * STEPS / KS, (ks + 1) * STEPS / KS>(
+              [&](auto S_) { red_step(std::integral_constant<int, ch - 1>{}, S_); });
+          if constexpr (ks == KS - 1) finalize(std::integral_constant<int, ch - 1>{});
+        }
+      }
+    });
+    static_for<0, STEPS>([&](auto S_) { red_step(std::integral_constant<int, NCH - 1>{}, S_); });
+    finalize(std::integral_constant<int, NCH - 1>{});
+  };
+
   auto tile = [&](int kt0, const char *cur) {
     float out[NSUB][NV];
     // (DI = 256 keeps one code path: its 128 query registers leave no room
     // for two instantiations of the sub-tile)
     if (DI <= 128 && kt0 + KT - 1 <= qw0 && qw0 + kQW - 1 <= qw_last) {
-      // whole tile below the wave's first query: no masks, no branches, so
-      // the sub-tiles' MFMAs and reductions interleave
-      if constexpr (DI <= 128) {
-#pragma unroll
-        for (int sb = 0; sb < NSUB; ++sb)
-          subtile(cur, sb, kt0 + sb * 64, out[sb], std::true_type{});
-      }
+      if constexpr (DI <= 128) full_tile(cur, out);
     } else {
 #pragma unroll
       for (int sb = 0; sb < NSUB; ++sb) {
