@@ -97,6 +97,14 @@ def build(verbose: bool = False) -> str:
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
+    # A kernel whose host stub was not emitted leaves an undefined symbol that
+    # only shows when the library is loaded: load it (in a child process, all
+    # symbols resolved now) before it replaces the previous build.
+    chk = subprocess.run([sys.executable, "-c",
+                          "import ctypes, os, sys; ctypes.CDLL(sys.argv[1], mode=os.RTLD_NOW)", tmp],
+                         capture_output=True, text=True)
+    if chk.returncode != 0:
+        raise RuntimeError(f"built library does not load:\n{chk.stderr}")
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}")

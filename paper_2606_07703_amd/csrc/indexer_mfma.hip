@@ -32,6 +32,10 @@ namespace {
 constexpr int kQW = 64;     // queries per wave
 constexpr int kKC = 1024;   // keys per workgroup chunk (rows kernel)
 constexpr int kXcds = 8;    // XCDs of the chip; workgroup i runs on XCD i % 8
+constexpr int kIdxBufferDword3 = 0x00020000;   // raw buffer resource: 32-bit data format
+// Waits until this wave's vector memory operations (direct-to-LDS key tile
+// loads and stores) have completed; LDS and scalar counters are not checked.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 template <int DI>
 struct Tile {
@@ -162,6 +166,41 @@ struct KeyStageT {
   }
 };
 
+// Direct-to-LDS loads of one key tile of the block kernel: slot c of padded
+// row r at byte (r * SLOTS + c) * 16, so chunk q of 64 slots is 1 KiB at
+// q * 1024, and wave w issues chunks w, w + NW, ... A lane's offset within a
+// tile is fixed (kept in registers); lanes on the padding slot load the
+// row's first 16 bytes into it (nothing reads it). Keys past S - 1 fall
+// outside the buffer and load zeros (they are always masked).
+template <int DI, int KT, int RB, int NW>
+struct KeyTileDma {
+  static constexpr int SLOTS = DI / 8 + 1, CHUNKS = KT * SLOTS / 64;
+  static constexpr int CPW = (CHUNKS + NW - 1) / NW;
+  static_assert(KT * SLOTS % 64 == 0 && SLOTS * 16 == RB, "whole chunks of padded rows");
+  __device__ __forceinline__ static void offsets(int wave, int lane, uint32_t (&koff)[CPW]) {
+#pragma unroll
+    for (int p = 0; p < CPW; ++p) {
+      const int slot = (wave + p * NW) * 64 + lane;
+      const int row = slot / SLOTS, col = slot % SLOTS;
+      koff[p] = (uint32_t)row * (DI * 2) + (uint32_t)(col < SLOTS - 1 ? col : 0) * 16;
+    }
+  }
+  __device__ __forceinline__ static void issue(uint32_t base, const uint16_t *ki, int S, int k0,
+                                               int wave, const uint32_t (&koff)[CPW]) {
+    const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(ki), (short)0,
+                                                      (uint32_t)S * (DI * 2), kIdxBufferDword3);
+    const uint32_t sb = (uint32_t)k0 * (DI * 2);
+#pragma unroll
+    for (int p = 0; p < CPW; ++p) {
+      const int q = wave + p * NW;
+      if (CHUNKS % NW == 0 || q < CHUNKS)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rs, (__attribute__((address_space(3))) void *)(size_t)(base + q * 1024), 16,
+            koff[p] + sb, 0, 0, 0);
+    }
+  }
+};
+
 // Half-wave combine on 32x32 MFMA outputs: lane l with lane l ^ 32.
 template <class Op>
 __device__ __forceinline__ float half_combine(float x, Op op) {
@@ -205,9 +244,15 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
   int qw0 = 0, qw_last = -1;   // qw_last < qw0 when the wave is past the end
   bf16x8 a[2][KS];
 
-  KeyStageT<DI, KT, RB, NT> stage;
-  stage.load(ki, S, uc.t * KT, tid);
-  stage.store(lds[0], tid);
+  using Dma = KeyTileDma<DI, KT, RB, NW>;
+  uint32_t koff[Dma::CPW];
+  Dma::offsets(wave, lane, koff);
+  const uint32_t lds_base = (uint32_t)(size_t)(__attribute__((address_space(3))) char *)&lds[0][0];
+  auto issue_keys = [&](int b, int k0) {   // into buffer b
+    Dma::issue(lds_base + b * T::BYTES, ki, S, k0, wave, koff);
+  };
+  issue_keys(0, uc.t * KT);
+  wait_vmem();
   __syncthreads();
 
   const float neutral = agg == SP_AGG_MAX ? -INFINITY : 0.f;
@@ -396,8 +441,20 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
     finalize(std::integral_constant<int, NCH - 1>{});
   };
 
-  auto tile = [&](int kt0, const char *cur) {
-    float out[NSUB][NV];
+  // Stores of a tile's block values (b <= 64); issued one tile late so that
+  // the wait for the next key tile's loads does not wait for them.
+  auto store_tile = [&](const float (&o)[NSUB][NV], int kt0, int qw0_) {
+#pragma unroll
+    for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int s = kt0 + sb * 64 + v_key(v);
+        const int tb0 = qw0_ + v_block(v) * BQ;          // first query of the block
+        const int tb1 = min(tb0 + BQ, S) - 1;
+        if (tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = o[sb][v];
+      }
+  };
+  auto tile = [&](int kt0, const char *cur, float (&out)[NSUB][NV]) {
     // (DI = 256 keeps one code path: its 128 query registers leave no room
     // for two instantiations of the sub-tile)
     if (DI <= 128 && kt0 + KT - 1 <= qw0 && qw0 + kQW - 1 <= qw_last) {
@@ -411,17 +468,7 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
         if (ks0 <= qw_last) subtile(cur, sb, ks0, out[sb], std::false_type{});
       }
     }
-    if constexpr (BQ <= kQW) {
-#pragma unroll
-      for (int sb = 0; sb < NSUB; ++sb)
-#pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          const int s = kt0 + sb * 64 + v_key(v);
-          const int tb0 = qw0 + v_block(v) * BQ;          // first query of the block
-          const int tb1 = min(tb0 + BQ, S) - 1;
-          if (tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = out[sb][v];
-        }
-    } else {
+    if constexpr (BQ > kQW) {
       // BQ = 128: waves 2i and 2i+1 hold the two halves of one block.
       if (wave & 1) {
 #pragma unroll
@@ -440,6 +487,8 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
       }
     }
   };
+  float pend[NSUB][NV];   // block values of the last tile, stored one tile late (b <= 64)
+  int pend_kt0 = -1, pend_qw0 = 0;
   // groups of the run; the key pipeline runs on across group boundaries
   for (int u = u0; u < u1;) {
     const int group = uc.qg, nt = uc.nt;
@@ -454,16 +503,21 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
     }
     const int t_end = min(nt, uc.t + (u1 - u));
     for (int t = uc.t; t < t_end; ++t, ++u) {
-      const bool more = u + 1 < u1;
-      if (more) stage.load(ki, S, t + 1 < nt ? (t + 1) * KT : 0, tid);
-      tile(t * KT, lds[(u - u0) & 1]);
-      if (more) stage.store(lds[(u - u0 + 1) & 1], tid);
+      if (u + 1 < u1) issue_keys((u - u0 + 1) & 1, t + 1 < nt ? (t + 1) * KT : 0);
+      if constexpr (BQ <= kQW)
+        if (pend_kt0 >= 0) store_tile(pend, pend_kt0, pend_qw0);
+      tile(t * KT, lds[(u - u0) & 1], pend);
+      pend_kt0 = t * KT;
+      pend_qw0 = qw0;
+      // the next tile's keys (and the stores of the tile before) have landed
+      wait_vmem();
       __syncthreads();
     }
     uc.qg = group + 1;
     uc.t = 0;
     uc.nt = UnitCursor<QG, KT>::tiles(S, group + 1);
   }
+  if constexpr (BQ <= kQW) store_tile(pend, pend_kt0, pend_qw0);
 }
 
 template <int DI, bool VEC>
