@@ -359,60 +359,85 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
   auto v_key = [&](int v) { return BPW == 1 ? 32 * h + n : 32 * (v / (BPW / 2)) + n; };
   auto v_block = [&](int v) { return BPW == 1 ? 0 : 2 * (v % (BPW / 2)) + h; };
 
+  // Stores of a tile's block values (b <= 64); issued one tile late so that
+  // the wait for the next key tile's loads does not wait for them.
+  auto store_tile = [&](const float (&o)[NSUB][NV], int kt0, int qw0_) {
+#pragma unroll
+    for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int s = kt0 + sb * 64 + v_key(v);
+        const int tb0 = qw0_ + v_block(v) * BQ;          // first query of the block
+        const int tb1 = min(tb0 + BQ, S) - 1;
+        if (tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = o[sb][v];
+      }
+  };
   // Tile wholly below the wave's first query (no masks): its 2 NSUB chains of
   // 32 keys (sub-tile sb, key tile ct) form one stream of operand reads and
   // products, and the reduction of each chain runs interleaved with the
   // products of the next, one (query tile, row group) step per operand read,
-  // so the vector work issues while the matrix core runs. Only the last
-  // chain's reduction follows the products.
-  auto full_tile = [&](const char *cur, float (&out)[NSUB][NV]) {
-    constexpr int NCH = 2 * NSUB, NR = NCH * KS, PF = 2, NBF = PF + 1, STEPS = 8;
-    f32x16 acc[2][2];
-    float vals[2][BPW];
+  // so the vector work issues while the matrix core runs. With DEFER (b <= 64)
+  // the last chain's reduction is carried into the next such tile's first
+  // chain (the tile-end barrier then does not wait for it); otherwise it
+  // follows the products.
+  constexpr int NCH = 2 * NSUB, STEPS = 8;
+  f32x16 facc[2][2] = {};   // accumulators of chains of even / odd index
+  float fvals[2][BPW];    // their block values
+  // step st of chain pc's reduction: query tile st / 4, row group st % 4
+  auto red_step = [&](auto pc_, auto st_) {
+    constexpr int pc = decltype(pc_)::value, st = decltype(st_)::value;
+    constexpr int c = pc & 1, qt = st >> 2, i = st & 3;
+    if constexpr (st == 0) {
+#pragma unroll
+      for (int bb = 0; bb < BPW; ++bb) fvals[c][bb] = neutral;
+    }
+    float x[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      x[r] = facc[c][qt][4 * i + r];
+      if constexpr (!MAXPOS) {
+        x[r] *= scale;
+        if (relu) x[r] = fmaxf(x[r], 0.f);
+      }
+    }
+    constexpr int bb = BPW == 1 ? 0 : (qt * 32 + i * 8) / BQ;
+    fvals[c][bb] = op(fvals[c][bb], op(op(x[0], x[1]), op(x[2], x[3])));
+  };
+  // chain pc done: combine the half-waves and keep this lane's values in o
+  auto finalize = [&](auto pc_, float (&o)[NSUB][NV]) {
+    constexpr int pc = decltype(pc_)::value, c = pc & 1, sb = pc >> 1, ct = pc & 1;
+#pragma unroll
+    for (int bb = 0; bb < BPW; ++bb) {
+      float m = half_combine(fvals[c][bb], op);
+      if constexpr (MAXPOS) {
+        m *= scale;
+        if (relu) m = fmaxf(m, 0.f);
+      }
+      fvals[c][bb] = m;
+    }
+    if constexpr (BPW == 1) {
+      if constexpr (ct == 0) o[sb][0] = fvals[c][0];
+      else o[sb][0] = h ? fvals[c][0] : o[sb][0];
+    } else {
+#pragma unroll
+      for (int m = 0; m < BPW / 2; ++m)
+        o[sb][ct * (BPW / 2) + m] = h ? fvals[c][2 * m + 1] : fvals[c][2 * m];
+    }
+  };
+  using LastChain = std::integral_constant<int, NCH - 1>;
+  // the carried reduction, on its own (before a masked tile, at the end)
+  auto flush = [&](float (&o)[NSUB][NV]) {
+    static_for<0, STEPS>([&](auto S_) { red_step(LastChain{}, S_); });
+    finalize(LastChain{}, o);
+  };
+  int pend_kt0 = -1, pend_qw0 = 0;   // tile and query base of the values in pend
+  auto full_tile = [&](const char *cur, float (&out)[NSUB][NV], float (&prev)[NSUB][NV],
+                       bool carry, auto defer_) {
+    constexpr bool DEFER = decltype(defer_)::value;
+    constexpr int NR = NCH * KS, PF = 2, NBF = PF + 1;
     bf16x8 kb[NBF];
     const uint32_t kbase =
         (uint32_t)(size_t)(const __attribute__((address_space(3))) char *)(cur + n * RB + h * 16);
-    // step st of chain pc's reduction: query tile st / 4, row group st % 4
-    auto red_step = [&](auto pc_, auto st_) {
-      constexpr int pc = decltype(pc_)::value, st = decltype(st_)::value;
-      constexpr int c = pc & 1, qt = st >> 2, i = st & 3;
-      if constexpr (st == 0) {
-#pragma unroll
-        for (int bb = 0; bb < BPW; ++bb) vals[c][bb] = neutral;
-      }
-      float x[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        x[r] = acc[c][qt][4 * i + r];
-        if constexpr (!MAXPOS) {
-          x[r] *= scale;
-          if (relu) x[r] = fmaxf(x[r], 0.f);
-        }
-      }
-      constexpr int bb = BPW == 1 ? 0 : (qt * 32 + i * 8) / BQ;
-      vals[c][bb] = op(vals[c][bb], op(op(x[0], x[1]), op(x[2], x[3])));
-    };
-    // chain pc done: combine the half-waves and keep this lane's values
-    auto finalize = [&](auto pc_) {
-      constexpr int pc = decltype(pc_)::value, c = pc & 1, sb = pc >> 1, ct = pc & 1;
-#pragma unroll
-      for (int bb = 0; bb < BPW; ++bb) {
-        float m = half_combine(vals[c][bb], op);
-        if constexpr (MAXPOS) {
-          m *= scale;
-          if (relu) m = fmaxf(m, 0.f);
-        }
-        vals[c][bb] = m;
-      }
-      if constexpr (BPW == 1) {
-        if constexpr (ct == 0) out[sb][0] = vals[c][0];
-        else out[sb][0] = h ? vals[c][0] : out[sb][0];
-      } else {
-#pragma unroll
-        for (int m = 0; m < BPW / 2; ++m)
-          out[sb][ct * (BPW / 2) + m] = h ? vals[c][2 * m + 1] : vals[c][2 * m];
-      }
-    };
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     static_for<0, NR + PF>([&](auto I) {
       constexpr int x = decltype(I)::value;
@@ -429,37 +454,49 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
         asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(kb[y % NBF]) : "i"(later));
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt)
-          acc[c][qt] = mfma32(a[qt][ks], kb[y % NBF], ks == 0 ? f32x16{} : acc[c][qt]);
+          facc[c][qt] = mfma32(a[qt][ks], kb[y % NBF], ks == 0 ? f32x16{} : facc[c][qt]);
         if constexpr (ch >= 1) {
           static_for<ks * STEPS / KS, (ks + 1) * STEPS / KS>(
               [&](auto S_) { red_step(std::integral_constant<int, ch - 1>{}, S_); });
-          if constexpr (ks == KS - 1) finalize(std::integral_constant<int, ch - 1>{});
+          if constexpr (ks == KS - 1) finalize(std::integral_constant<int, ch - 1>{}, out);
+        } else if constexpr (DEFER) {
+          // the previous tile's last chain (odd accumulators): reduced here
+          // whether or not it is pending, stored only if it is
+          static_for<ks * STEPS / KS, (ks + 1) * STEPS / KS>(
+              [&](auto S_) { red_step(LastChain{}, S_); });
+          if constexpr (ks == KS - 1) {
+            finalize(LastChain{}, prev);
+            if (carry) store_tile(prev, pend_kt0, pend_qw0);
+          }
         }
       }
     });
-    static_for<0, STEPS>([&](auto S_) { red_step(std::integral_constant<int, NCH - 1>{}, S_); });
-    finalize(std::integral_constant<int, NCH - 1>{});
+    if constexpr (!DEFER) flush(out);
   };
 
-  // Stores of a tile's block values (b <= 64); issued one tile late so that
-  // the wait for the next key tile's loads does not wait for them.
-  auto store_tile = [&](const float (&o)[NSUB][NV], int kt0, int qw0_) {
-#pragma unroll
-    for (int sb = 0; sb < NSUB; ++sb)
-#pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const int s = kt0 + sb * 64 + v_key(v);
-        const int tb0 = qw0_ + v_block(v) * BQ;          // first query of the block
-        const int tb1 = min(tb0 + BQ, S) - 1;
-        if (tb0 < S && s <= tb1) Y[(size_t)(tb0 / BQ) * S + s] = o[sb][v];
-      }
-  };
-  auto tile = [&](int kt0, const char *cur, float (&out)[NSUB][NV]) {
+  // One key tile; prev holds the values of the tile before (b <= 64: stored
+  // here, after its carried chain is reduced if carry). Returns whether this
+  // tile's last chain is carried.
+  auto tile = [&](int kt0, const char *cur, float (&out)[NSUB][NV], float (&prev)[NSUB][NV],
+                  bool carry) -> bool {
     // (DI = 256 keeps one code path: its 128 query registers leave no room
     // for two instantiations of the sub-tile)
-    if (DI <= 128 && kt0 + KT - 1 <= qw0 && qw0 + kQW - 1 <= qw_last) {
-      if constexpr (DI <= 128) full_tile(cur, out);
+    const bool full = DI <= 128 && kt0 + KT - 1 <= qw0 && qw0 + kQW - 1 <= qw_last;
+    if (full) {
+      if constexpr (DI <= 128) {
+        if constexpr (BQ <= kQW) {
+          if (!carry && pend_kt0 >= 0) store_tile(prev, pend_kt0, pend_qw0);
+          full_tile(cur, out, prev, carry, std::true_type{});
+        } else {
+          full_tile(cur, out, prev, false, std::false_type{});
+        }
+      }
     } else {
+      if constexpr (BQ <= kQW) {
+        if constexpr (DI <= 128)
+          if (carry) flush(prev);
+        if (pend_kt0 >= 0) store_tile(prev, pend_kt0, pend_qw0);
+      }
 #pragma unroll
       for (int sb = 0; sb < NSUB; ++sb) {
         const int ks0 = kt0 + sb * 64;
@@ -486,9 +523,10 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
         }
       }
     }
+    return BQ <= kQW && full;
   };
   float pend[NSUB][NV];   // block values of the last tile, stored one tile late (b <= 64)
-  int pend_kt0 = -1, pend_qw0 = 0;
+  bool carry = false;     // its last chain's reduction is still pending
   // groups of the run; the key pipeline runs on across group boundaries
   for (int u = u0; u < u1;) {
     const int group = uc.qg, nt = uc.nt;
@@ -504,9 +542,12 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
     const int t_end = min(nt, uc.t + (u1 - u));
     for (int t = uc.t; t < t_end; ++t, ++u) {
       if (u + 1 < u1) issue_keys((u - u0 + 1) & 1, t + 1 < nt ? (t + 1) * KT : 0);
-      if constexpr (BQ <= kQW)
-        if (pend_kt0 >= 0) store_tile(pend, pend_kt0, pend_qw0);
-      tile(t * KT, lds[(u - u0) & 1], pend);
+      float out[NSUB][NV];
+      carry = tile(t * KT, lds[(u - u0) & 1], out, pend, carry);
+#pragma unroll
+      for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+        for (int v = 0; v < NV; ++v) pend[sb][v] = out[sb][v];
       pend_kt0 = t * KT;
       pend_qw0 = qw0;
       // the next tile's keys (and the stores of the tile before) have landed
@@ -517,7 +558,11 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
     uc.t = 0;
     uc.nt = UnitCursor<QG, KT>::tiles(S, group + 1);
   }
-  if constexpr (BQ <= kQW) store_tile(pend, pend_kt0, pend_qw0);
+  if constexpr (BQ <= kQW) {
+    if constexpr (DI <= 128)
+      if (carry) flush(pend);
+    store_tile(pend, pend_kt0, pend_qw0);
+  }
 }
 
 template <int DI, bool VEC>
