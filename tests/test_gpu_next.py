@@ -132,7 +132,8 @@ def _project(S, dm, di, pos0, seed, theta=10000.0, eps=1e-6):
 
 @pytest.mark.parametrize("S,dm,di,pos0", [(1, 64, 64, 0), (130, 128, 64, 0),
                                           (130, 192, 128, 1000), (65, 256, 256, 7),
-                                          (200, 512, 128, 100000)])
+                                          (200, 512, 128, 100000), (300, 1024, 64, 5),
+                                          (385, 4096, 128, 0)])
 def test_indexer_project(S, dm, di, pos0):
     say(f"project S={S} d_model={dm} d_idx={di} pos0={pos0}")
     (x, wq, wk, gamma, beta), qo, ko = _project(S, dm, di, pos0, seed=S + di)
@@ -153,7 +154,7 @@ def test_indexer_project_full_size_sampled():
     S, dm, di = 32768, 4096, 128
     say(f"project full size S={S} d_model={dm} d_idx={di}")
     (x, wq, wk, gamma, beta), qo, ko = _project(S, dm, di, 0, seed=4)
-    sample = np.array([0, 1, 63, 64, 4095, 20000, 32704, 32767])
+    sample = np.array([0, 1, 63, 64, 127, 128, 255, 4095, 20000, 32640, 32704, 32767])
     rq, rk = oracle.project(x, wq, wk, gamma, beta, rows=sample)
     _check_proj(qo[sample], rq)
     _check_proj(ko[sample], rk)
