@@ -133,7 +133,8 @@ def _project(S, dm, di, pos0, seed, theta=10000.0, eps=1e-6):
 @pytest.mark.parametrize("S,dm,di,pos0", [(1, 64, 64, 0), (130, 128, 64, 0),
                                           (130, 192, 128, 1000), (65, 256, 256, 7),
                                           (200, 512, 128, 100000), (300, 1024, 64, 5),
-                                          (385, 4096, 128, 0)])
+                                          (385, 4096, 128, 0), (129, 64, 128, 0),
+                                          (257, 128, 128, 9)])
 def test_indexer_project(S, dm, di, pos0):
     say(f"project S={S} d_model={dm} d_idx={di} pos0={pos0}")
     (x, wq, wk, gamma, beta), qo, ko = _project(S, dm, di, pos0, seed=S + di)
