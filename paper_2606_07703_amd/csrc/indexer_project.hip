@@ -221,27 +221,29 @@ __global__ __launch_bounds__(kPW * 64) void project_kernel(
 // Wide kernel for d_idx <= 128: 128 tokens per workgroup, so at 32K tokens
 // one round of 256 workgroups covers the chip and each W tile read from L2
 // serves twice the tokens. x, W_Q and W_K tiles of 32 model columns go
-// straight from memory into padded LDS rows (16-byte slots, one padding slot
-// per row) in a ring of kWStages stages, kWStages - 2 of them in flight
-// behind the one being multiplied. Eight waves (two token halves by four
+// straight from memory into LDS rows of four 16-byte slots, stored at slot
+// c ^ ((row >> 1) & 3) so that eight consecutive rows read at one slot hit
+// distinct banks, in a ring of kWStages stages, kWStages - 2 of them in
+// flight behind the one being multiplied. Eight waves (two token halves by four
 // output quarters) run v_mfma_f32_32x32x16_bf16 with tokens as A rows and
 // output columns as B rows; the operand reads are inline so the compiler
 // adds no wait for the direct loads still in flight.
 constexpr int kWT = 128;        // tokens per workgroup
 constexpr int kWK = 32;         // model columns per stage
 constexpr int kWW = 8;          // waves
-constexpr int kWStages = 5;
+constexpr int kWStages = 6;
 constexpr int kProjBufferDword3 = 0x00020000;   // raw buffer resource: 32-bit data format
 
 template <int DI>
 struct WideLayout {
   static constexpr int N = 2 * DI;                   // output columns (q then k)
-  static constexpr int SLOTS = kWK / 8 + 1;          // 16-byte slots per padded row
-  static constexpr int RB = SLOTS * 16;              // padded row bytes (80)
+  static constexpr int SLOTS = kWK / 8;              // 16-byte slots per row
+  static constexpr int RB = SLOTS * 16;              // row bytes (64)
   static constexpr int XCH = kWT * SLOTS / 64;       // 1 KiB direct loads per stage: x
   static constexpr int QCH = DI * SLOTS / 64;        // ... W_Q (and as many for W_K)
   static constexpr int CH = XCH + 2 * QCH;
   static constexpr int CPW = (CH + kWW - 1) / kWW;   // per wave; surplus ones repeat a chunk
+  static_assert(SLOTS == 4, "the swizzle permutes four slots");
   static constexpr int XBYTES = kWT * RB;
   static constexpr int STAGE = (kWT + N) * RB;
   static constexpr int NB = N / 4 / 32;              // 32-column output blocks per wave
@@ -257,10 +259,10 @@ struct WideLayout {
 constexpr int vm_wait_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
 // Direct loads of one stage. Chunk q of a stage covers 64 consecutive slots
-// of one array's padded rows; lane l of chunk q writes LDS bytes
-// [1024 q + 16 l, + 16). A lane on a padding slot loads its row's first 16
-// bytes, which nothing reads. Token rows past the sequence end read the last
-// row (their outputs are not written).
+// of one array's rows; lane l of chunk q writes LDS bytes [1024 q + 16 l,
+// + 16), which hold row (64 q + l) / 4 at column slot ((64 q + l) % 4) ^
+// swizzle(row). Token rows past the sequence end read the last row (their
+// outputs are not written).
 template <int DI>
 struct WideDma {
   using L = WideLayout<DI>;
@@ -271,8 +273,8 @@ struct WideDma {
     for (int p = 0; p < L::CPW; ++p) {
       const int q = chunk(wave, p);
       const int q0 = q < L::XCH ? q : (q - L::XCH) % L::QCH;
-      const int slot = q0 * 64 + lane, row = slot / L::SLOTS, c = slot % L::SLOTS;
-      const uint32_t cb = (uint32_t)(c < L::SLOTS - 1 ? c : 0) * 16;
+      const int slot = q0 * 64 + lane, row = slot / L::SLOTS;
+      const uint32_t cb = (uint32_t)((slot % L::SLOTS) ^ ((row >> 1) & 3)) * 16;
       const int r = q < L::XCH ? min(t0 + row, S - 1) : row;
       off[p] = (uint32_t)r * (uint32_t)dm * 2u + cb;
     }
@@ -326,9 +328,13 @@ __global__ __launch_bounds__(kWW * 64) void project_wide_kernel(
   for (int bt = 0; bt < 2; ++bt)
 #pragma unroll
     for (int bo = 0; bo < NB; ++bo) acc[bt][bo] = f32x16{};
-  // per-lane LDS offsets within a stage: A rows (tokens), B rows (outputs)
-  const uint32_t xrow = (uint32_t)(wt * 64 + n) * RB + h * 16;
-  const uint32_t wrow = (uint32_t)L::XBYTES + (uint32_t)(wo * NB * 32 + n) * RB + h * 16;
+  // per-lane LDS offsets within a stage: A rows (tokens), B rows (outputs);
+  // row bases are multiples of 32, so a lane's swizzle is (n >> 1) & 3, and
+  // k-step ks reads column slot 2 ks + h
+  const uint32_t sw = (uint32_t)((n >> 1) & 3);
+  const uint32_t xrow = (uint32_t)(wt * 64 + n) * RB;
+  const uint32_t wrow = (uint32_t)L::XBYTES + (uint32_t)(wo * NB * 32 + n) * RB;
+  const uint32_t kso[2] = {((uint32_t)h ^ sw) * 16, (((uint32_t)h + 2) ^ sw) * 16};
   for (int it = 0; it < nk; ++it) {
     // this wave's loads of stage it have landed (later stages may still fly)
     if (it + NS - 2 < nk)
@@ -344,20 +350,20 @@ __global__ __launch_bounds__(kWW * 64) void project_wide_kernel(
       Dma::issue(lds0 + ((it + NS - 1) % NS) * L::STAGE, (it + NS - 1) * kWK, S, dm, x, wq, wk,
                  wave, off);
     const uint32_t sbase = lds0 + (it % NS) * L::STAGE;
-    const uint32_t xa = sbase + xrow, wa = sbase + wrow;
     bf16x8 fa[KS][2], fb[KS][NB];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
+      const uint32_t xa = sbase + xrow + kso[ks], wa = sbase + wrow + kso[ks];
 #pragma unroll
       for (int bt = 0; bt < 2; ++bt)
         asm volatile("ds_read_b128 %0, %1 offset:%2"
                      : "=v"(fa[ks][bt])
-                     : "v"(xa), "i"(bt * 32 * RB + ks * 32));
+                     : "v"(xa), "i"(bt * 32 * RB));
 #pragma unroll
       for (int bo = 0; bo < NB; ++bo)
         asm volatile("ds_read_b128 %0, %1 offset:%2"
                      : "=v"(fb[ks][bo])
-                     : "v"(wa), "i"(bo * 32 * RB + ks * 32));
+                     : "v"(wa), "i"(bo * 32 * RB));
     }
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
