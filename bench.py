@@ -1,8 +1,9 @@
-"""Benchmark: causal top-k sparse GQA prefill at 32K on one MI355X.
+"""Benchmark: causal top-k sparse GQA prefill on one MI355X.
 
-Workload "headline_32k": S=32768, Hq=32, Hkv=8, d=128, d_idx=128, top-k 2048,
-bf16, seeded synthetic inputs with 128 planted needles. One step runs every
-stage of the path once, on one HIP stream, with inputs resident in HBM:
+Default workload "headline_32k": S=32768, Hq=32, Hkv=8, d=128, d_idx=128,
+top-k 2048, bf16, seeded synthetic inputs with 128 planted needles. One step
+runs every stage of the path once, on one HIP stream, with inputs resident
+in HBM:
 
   1. indexer mode, 64-query selection blocks: scores -> top-k -> sparse attn
   2. indexer mode, per-query selection:       scores -> top-k -> sparse attn,
@@ -17,10 +18,21 @@ stage of the path once, on one HIP stream, with inputs resident in HBM:
 
 `value` is the ms per layer of (1), the selection-block-shared sparse prefill;
 the per-query and oracle-mode times, the dense time and the speedups are
-reported beside it. Every stage is bracketed by HIP events on the launch
-stream; per-stage times are medians over the timed steps.
+reported beside it.
 
-Prints one JSON line. Only one GPU is used: --gpus above 1 exits.
+--workload picks another of the paper-shaped workloads, each with its own
+selection and modes (one JSON line each; --workload all runs every one):
+
+  oracle_tiny_512  fp32 oracle mode, per query, k=64 (value: oracle mode)
+  indexer_4k       indexer per query, k=512, unfused and fused (value: unfused)
+  block_16k        64-query blocks, k=2048, 128-token forced window, summed
+                   (value) and max-aggregated scores
+  stress_100k      102,400 tokens, 128-query blocks, k=4096, planted (value)
+                   and untrained indexer vectors
+
+Every stage is bracketed by HIP events on the launch stream; per-stage times
+are medians over the timed steps, roofline figures use the mean launch time.
+Prints one JSON line per workload. Only one GPU is used: --gpus above 1 exits.
 """
 from __future__ import annotations
 
@@ -36,12 +48,18 @@ sys.path.insert(0, ROOT)
 import numpy as np  # noqa: E402
 import torch  # noqa: E402
 
-from paper_2606_07703_amd.traffic import stage_traffic  # noqa: E402
+from paper_2606_07703_amd.traffic import stage_counters, stage_traffic  # noqa: E402
 
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "traffic_headline_32k.md")
+PROFILES = os.path.join(ROOT, "profiles")
+TRAFFIC_SUMMARY = os.path.join(PROFILES, "traffic_headline_32k.md")
+MFMA_SUMMARY = os.path.join(PROFILES, "mfma_headline_32k.md")
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 FP32_VALU_PEAK_TFLOPS = 157.3
+# fp64 rate of the oracle on a many-core host, used only to size CPU samples
+CPU_PLAN_FLOPS = 3e10
+METRIC = "ms/layer sparse GQA prefill @32K, speedup vs own dense, % HBM/MFMA roofline"
+ALL_WORKLOADS = ("oracle_tiny_512", "indexer_4k", "block_16k", "headline_32k", "stress_100k")
 
 
 def causal_pairs(S: int) -> int:
@@ -53,43 +71,219 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="headline_32k")
+    ap.add_argument("--workload", default="headline_32k",
+                    help="one of " + ", ".join(ALL_WORKLOADS) + ", or all")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-units", type=int, default=256,
-                    help="selection blocks the CPU oracle times (bounded sample)")
+    ap.add_argument("--cpu-seconds", type=float, default=8.0,
+                    help="rough CPU time per oracle leg (bounded samples)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one device copy of this size (the calibration "
                          "kernel for rocprofv3 FETCH_SIZE/WRITE_SIZE runs)")
     return ap.parse_args()
 
 
-def support_rows(idx: torch.Tensor) -> int:
-    return int((idx >= 0).sum().item())
-
-
-def causal_support_pairs(idx: np.ndarray, S: int, b: int) -> int:
-    """Sum over queries t of |{s in idx[t//b] : 0 <= s <= t}|."""
-    total = 0
-    R, k = idx.shape
+def causal_support_pairs(idx: np.ndarray, S: int, b: int) -> np.ndarray:
+    """Per selection block r: sum over its queries t of |{s in idx[r] : 0 <= s <= t}|."""
+    R = idx.shape[0]
+    out = np.zeros(R, dtype=np.int64)
     for r in range(R):
         row = np.sort(idx[r][idx[r] >= 0])
         t0, t1 = r * b, min(r * b + b, S) - 1
-        ts = np.arange(t0, t1 + 1)
-        total += int(np.searchsorted(row, ts, side="right").sum())
-    return total
+        out[r] = int(np.searchsorted(row, np.arange(t0, t1 + 1), side="right").sum())
+    return out
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the path shards by selection blocks, see the design notes)", file=sys.stderr)
-        sys.exit(2)
+class Plan:
+    """Stages of one workload's step, their algorithmic work and the modes
+    (sums of stages) reported as ms/layer."""
+
+    def __init__(self, w):
+        self.w = w
+        self.stages = []       # (name, fn)
+        self.work = {}         # name -> (bound, flops or None, bytes or None) (filled after timing)
+        self.modes = {}        # mode -> [stage names]
+        self.value_mode = None
+        self.tables = {}       # stage prefix -> (idx tensor, b)
+        self.extra = {}
+
+    def add(self, name, fn):
+        self.stages.append((name, fn))
+
+
+def build_plan(w, dev, B, PL, make_inputs, make_projection_inputs):
+    S, Hq, Hkv, d, di, k = w.seq_len, w.num_q_heads, w.num_kv_heads, w.head_dim, w.index_dim, w.topk
+    plan = Plan(w)
+
+    def indexer_mode(prefix, b, agg="max", W=0, q_idx=None, k_idx=None, fused=False,
+                     paged=False):
+        p = B.Problem(S, Hq, Hkv, d, index_dim=di, topk=k, block_q=b, local_window=W, agg=agg,
+                      dtype=w.dtype)
+        buf = PL.Buffers.for_problem(p)
+        qi = dev.q_idx if q_idx is None else q_idx
+        ki = dev.k_idx if k_idx is None else k_idx
+        plan.add(f"{prefix}.indexer_scores", lambda: B.sp_indexer_scores(p, qi, ki, buf.scores))
+        plan.add(f"{prefix}.topk", lambda: B.sp_topk_select(p, buf.scores, buf.idx))
+        plan.add(f"{prefix}.sparse_attn",
+                 lambda: B.sp_sparse_gqa_attn(p, dev.q, dev.k, dev.v, buf.idx, buf.o))
+        plan.modes[prefix] = [f"{prefix}.indexer_scores", f"{prefix}.topk", f"{prefix}.sparse_attn"]
+        plan.tables[prefix] = (buf, b)
+        if paged:
+            # the same K/V scattered over a paged cache of 64-token pages
+            # (every logical page at a shuffled physical page, plus spares)
+            PAGE = 64
+            npg = (S + PAGE - 1) // PAGE
+            perm = torch.from_numpy(
+                np.random.default_rng(w.seed).permutation(npg + 8)[:npg].astype(np.int32))
+            pad = npg * PAGE - S
+            kk = torch.cat([dev.k, dev.k.new_zeros(pad, Hkv, d)]) if pad else dev.k
+            vv = torch.cat([dev.v, dev.v.new_zeros(pad, Hkv, d)]) if pad else dev.v
+            kpg = torch.zeros(npg + 8, PAGE, Hkv, d, dtype=dev.k.dtype, device="cuda")
+            vpg = torch.zeros_like(kpg)
+            kpg[perm.long().cuda()] = kk.view(npg, PAGE, Hkv, d)
+            vpg[perm.long().cuda()] = vv.view(npg, PAGE, Hkv, d)
+            ptab = perm.cuda()
+            o_paged = torch.empty_like(dev.q)
+            plan.add(f"{prefix}.sparse_attn_paged", lambda: B.sp_sparse_gqa_attn_paged(
+                p, dev.q, kpg, vpg, ptab, buf.idx, o_paged))
+        if fused:
+            fz_idx = torch.empty(S, k, dtype=torch.int32, device="cuda")
+            fz_ws = torch.empty(B.sp_workspace_bytes(p, "indexer_topk"), dtype=torch.uint8,
+                                device="cuda")
+            plan.add(f"{prefix}.fused_scores_topk",
+                     lambda: B.sp_indexer_topk(p, qi, ki, fz_idx, fz_ws))
+            plan.modes[prefix + "_fused"] = [f"{prefix}.fused_scores_topk", f"{prefix}.sparse_attn"]
+        return p, buf
+
+    def oracle_mode():
+        p = B.Problem(S, Hq, Hkv, d, topk=k, block_q=1, dtype=w.dtype)
+        buf = PL.Buffers.for_problem(p, oracle=True)
+        plan.add("oracle.normalisers",
+                 lambda: B.sp_dense_attn(p, dev.q, dev.k, dev.v, None, buf.lse))
+        plan.add("oracle.mass", lambda: B.sp_oracle_support(p, dev.q, dev.k, buf.lse, buf.scores))
+        plan.add("oracle.topk", lambda: B.sp_topk_select(p, buf.scores, buf.idx))
+        plan.add("oracle.sparse_attn",
+                 lambda: B.sp_sparse_gqa_attn(p, dev.q, dev.k, dev.v, buf.idx, buf.o))
+        plan.modes["oracle"] = ["oracle.normalisers", "oracle.mass", "oracle.topk",
+                                "oracle.sparse_attn"]
+        plan.tables["oracle"] = (buf, 1)
+        return p, buf
+
+    def dense():
+        p = B.Problem(S, Hq, Hkv, d, dtype=w.dtype)
+        o = torch.empty(S, Hq, d, dtype=dev.q.dtype, device="cuda")
+        plan.add("dense.attn", lambda: B.sp_dense_attn(p, dev.q, dev.k, dev.v, o, None))
+        plan.modes["dense"] = ["dense.attn"]
+
+    if w.name == "headline_32k":
+        # indexer front end on Qwen-like hidden states (d_model 4096, random weights)
+        D_MODEL = 4096
+        pb0 = B.Problem(S, Hq, Hkv, d, index_dim=di, topk=k, block_q=64, dtype=w.dtype)
+        px, pwq, pwk, pg, pbeta = (t.cuda() for t in make_projection_inputs(S, D_MODEL, di,
+                                                                           seed=w.seed))
+        pqo = torch.empty(S, di, dtype=torch.bfloat16, device="cuda")
+        pko = torch.empty(S, di, dtype=torch.bfloat16, device="cuda")
+        plan.add("frontend.project",
+                 lambda: B.sp_indexer_project(pb0, px, pwq, pwk, pg, pbeta, pqo, pko))
+        plan.extra["d_model"] = D_MODEL
+        indexer_mode("block64", 64, paged=True)
+        pq, buf_q = indexer_mode("perquery", 1, fused=True)
+        dense()
+        _, buf_o = oracle_mode()
+        # KL distillation objective: teacher = oracle mass rows, student =
+        # per-query indexer scores, every query row supervised
+        kl_rows = torch.arange(S, dtype=torch.int32, device="cuda")
+        kl_val = torch.empty(S, device="cuda")
+        kl_loss = torch.empty(1, device="cuda")
+        kl_grad = torch.empty(S, S, device="cuda")
+        plan.add("kl.loss", lambda: B.sp_kl_loss(pq, kl_rows, buf_o.scores, buf_q.scores, kl_val,
+                                                 kl_loss, kl_grad))
+        plan.value_mode = "block64"
+    elif w.name == "oracle_tiny_512":
+        oracle_mode()
+        dense()
+        plan.value_mode = "oracle"
+    elif w.name == "indexer_4k":
+        indexer_mode("perquery", 1, fused=True)
+        dense()
+        plan.value_mode = "perquery"
+    elif w.name == "block_16k":
+        indexer_mode("block64sum", 64, agg="sum", W=w.local_window)
+        indexer_mode("block64max", 64, agg="max", W=w.local_window)
+        dense()
+        plan.value_mode = "block64sum"
+    elif w.name == "stress_100k":
+        b = w.block_q[0]
+        indexer_mode(f"block{b}", b)
+        # untrained indexer: the same draws without the needles planted in
+        # k_idx (i.i.d. Gaussian vectors, uncorrelated with K)
+        un = make_inputs(S, Hq, Hkv, d, index_dim=di, dtype=w.dtype, needles=w.needles,
+                         stratified=w.stratified, seed=w.seed, untrained=True)
+        uq, uk = un.q_idx.cuda(), un.k_idx.cuda()
+        plan.extra["untrained"] = (un.q_idx, un.k_idx)
+        indexer_mode(f"untrained{b}", b, q_idx=uq, k_idx=uk)
+        dense()
+        plan.value_mode = f"block{b}"
+    else:
+        raise SystemExit(f"no bench plan for workload {w.name}")
+    return plan
+
+
+def work_model(plan, S, Hq, Hkv, d, di, k, elt):
+    """Algorithmic work per launch of each stage: (bound, flops, bytes). Counts
+    causal pairs and selected rows only, never the work the method avoids."""
+    C = causal_pairs(S)
+    work, counts = {}, {}
+    for name, _ in plan.stages:
+        prefix, stage = name.split(".", 1)
+        if stage == "project":
+            dm = plan.extra["d_model"]
+            work[name] = ("hbm", 2.0 * S * dm * 2 * di,
+                          2.0 * (S * dm + 2 * di * dm + 2 * S * di) + 8.0 * di)
+        elif stage == "attn" and prefix == "dense":
+            work[name] = ("mfma" if elt == 2 else "alu", 4.0 * d * Hq * C, None)
+        elif stage == "normalisers":
+            work[name] = ("mfma" if elt == 2 else "alu", 2.0 * d * Hq * C, None)
+        elif stage == "mass":
+            work[name] = ("mfma" if elt == 2 else "alu", 2.0 * d * Hq * C, 4.0 * C)
+        elif stage in ("indexer_scores", "topk", "sparse_attn", "sparse_attn_paged",
+                       "fused_scores_topk"):
+            buf, b = plan.tables[prefix]
+            R = (S + b - 1) // b
+            lens = np.minimum(np.arange(R) * b + b, S).astype(np.float64)
+            if stage == "indexer_scores":
+                if b == 1:
+                    work[name] = ("hbm", 2.0 * di * C, 4.0 * C + 2.0 * S * di * elt)
+                else:
+                    work[name] = ("mfma", 2.0 * di * C, None)
+            elif stage == "topk":
+                work[name] = ("hbm", None, 4.0 * lens.sum() + 4.0 * R * k)
+            elif stage == "fused_scores_topk":
+                # one scoring of every causal pair (the passes recompute it;
+                # that is overhead, not work)
+                work[name] = ("mfma", 2.0 * di * C, 2.0 * S * di * elt + 4.0 * S * k)
+            else:
+                if prefix not in counts:
+                    idx_np = buf.idx.cpu().numpy()
+                    counts[prefix] = (int((idx_np >= 0).sum()),
+                                      causal_support_pairs(idx_np, S, b), idx_np.size)
+                rows, pairs, nidx = counts[prefix]
+                gather = rows * Hkv * 2 * d * elt      # K and V rows of every KV head
+                qo = 2 * S * Hq * d * elt
+                work[name] = ("hbm", 4.0 * d * Hq * pairs.sum(), gather + qo + 4.0 * nidx)
+        elif stage == "loss":
+            # read P and z on s <= t, write the full gradient rows
+            work[name] = ("hbm", None, 2 * 4.0 * C + 4.0 * S * S + 8.0 * S)
+        else:
+            raise KeyError(name)
+    return work, counts
+
+
+def run_workload(args, name):
     from paper_2606_07703_amd import binding as B
     from paper_2606_07703_amd import pipeline as PL
     from synth import get_workload, make_inputs, make_projection_inputs
 
-    w = get_workload(args.workload)
+    w = get_workload(name)
     S, Hq, Hkv, d, di, k = w.seq_len, w.num_q_heads, w.num_kv_heads, w.head_dim, w.index_dim, w.topk
     torch.cuda.set_device(0)
     B.load()
@@ -97,62 +291,11 @@ def main():
     inp = make_inputs(S, Hq, Hkv, d, index_dim=di, dtype=w.dtype, needles=w.needles,
                       stratified=w.stratified, seed=w.seed)
     dev = inp.to("cuda")
-    print(f"[bench] inputs ready in {time.time() - t_gen:.1f}s", file=sys.stderr, flush=True)
-
-    pb = B.Problem(S, Hq, Hkv, d, index_dim=di, topk=k, block_q=64, dtype=w.dtype)
-    pq = B.Problem(S, Hq, Hkv, d, index_dim=di, topk=k, block_q=1, dtype=w.dtype)
-    buf_b = PL.Buffers.for_problem(pb)
-    buf_q = PL.Buffers.for_problem(pq)
-    buf_o = PL.Buffers.for_problem(pq, oracle=True)
-    o_dense = torch.empty(S, Hq, d, dtype=dev.q.dtype, device="cuda")
-    # KL distillation objective: teacher = oracle mass rows, student = per-query
-    # indexer scores, every query row supervised
-    kl_rows = torch.arange(S, dtype=torch.int32, device="cuda")
-    kl_val = torch.empty(S, device="cuda")
-    kl_loss = torch.empty(1, device="cuda")
-    kl_grad = torch.empty(S, S, device="cuda")
-    # the same K/V scattered over a paged cache of 64-token pages (every
-    # logical page at a shuffled physical page, plus spare pages)
-    PAGE = 64
-    npg = (S + PAGE - 1) // PAGE
-    perm = torch.from_numpy(np.random.default_rng(w.seed).permutation(npg + 8)[:npg].astype(np.int32))
-    kpg = torch.zeros(npg + 8, PAGE, Hkv, d, dtype=dev.k.dtype, device="cuda")
-    vpg = torch.zeros_like(kpg)
-    kpg[perm.long().cuda()] = dev.k.view(npg, PAGE, Hkv, d)
-    vpg[perm.long().cuda()] = dev.v.view(npg, PAGE, Hkv, d)
-    ptab = perm.cuda()
-    o_paged = torch.empty_like(dev.q)
-    # fused per-query scoring + top-k (no S x S score buffer)
-    fz_idx = torch.empty(S, k, dtype=torch.int32, device="cuda")
-    fz_ws = torch.empty(B.sp_workspace_bytes(pq, "indexer_topk"), dtype=torch.uint8,
-                        device="cuda")
-    # indexer front end on Qwen-like hidden states (d_model 4096, random weights)
-    D_MODEL = 4096
-    px, pwq, pwk, pg, pb_ = (t.cuda() for t in make_projection_inputs(S, D_MODEL, di, seed=w.seed))
-    pqo = torch.empty(S, di, dtype=torch.bfloat16, device="cuda")
-    pko = torch.empty(S, di, dtype=torch.bfloat16, device="cuda")
+    print(f"[bench] {name}: inputs ready in {time.time() - t_gen:.1f}s", file=sys.stderr,
+          flush=True)
+    plan = build_plan(w, dev, B, PL, make_inputs, make_projection_inputs)
     stream = torch.cuda.current_stream()
-
-    stages = [
-        ("frontend.project", lambda: B.sp_indexer_project(pb, px, pwq, pwk, pg, pb_, pqo, pko)),
-        ("block64.indexer_scores", lambda: B.sp_indexer_scores(pb, dev.q_idx, dev.k_idx, buf_b.scores)),
-        ("block64.topk", lambda: B.sp_topk_select(pb, buf_b.scores, buf_b.idx)),
-        ("block64.sparse_attn", lambda: B.sp_sparse_gqa_attn(pb, dev.q, dev.k, dev.v, buf_b.idx, buf_b.o)),
-        ("block64.sparse_attn_paged", lambda: B.sp_sparse_gqa_attn_paged(
-            pb, dev.q, kpg, vpg, ptab, buf_b.idx, o_paged)),
-        ("perquery.indexer_scores", lambda: B.sp_indexer_scores(pq, dev.q_idx, dev.k_idx, buf_q.scores)),
-        ("perquery.topk", lambda: B.sp_topk_select(pq, buf_q.scores, buf_q.idx)),
-        ("perquery.sparse_attn", lambda: B.sp_sparse_gqa_attn(pq, dev.q, dev.k, dev.v, buf_q.idx, buf_q.o)),
-        ("perquery.fused_scores_topk", lambda: B.sp_indexer_topk(pq, dev.q_idx, dev.k_idx, fz_idx,
-                                                                 fz_ws)),
-        ("dense.attn", lambda: B.sp_dense_attn(pq, dev.q, dev.k, dev.v, o_dense, None)),
-        ("oracle.normalisers", lambda: B.sp_dense_attn(pq, dev.q, dev.k, dev.v, None, buf_o.lse)),
-        ("oracle.mass", lambda: B.sp_oracle_support(pq, dev.q, dev.k, buf_o.lse, buf_o.scores)),
-        ("oracle.topk", lambda: B.sp_topk_select(pq, buf_o.scores, buf_o.idx)),
-        ("oracle.sparse_attn", lambda: B.sp_sparse_gqa_attn(pq, dev.q, dev.k, dev.v, buf_o.idx, buf_o.o)),
-        ("kl.loss", lambda: B.sp_kl_loss(pq, kl_rows, buf_o.scores, buf_q.scores, kl_val, kl_loss,
-                                         kl_grad)),
-    ]
+    stages = plan.stages
 
     def step(events=None):
         for i, (_, fn) in enumerate(stages):
@@ -162,11 +305,10 @@ def main():
         if events is not None:
             events[-1].record(stream)
 
-    for i in range(args.warmup):
+    for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    print("[bench] warmup done", file=sys.stderr, flush=True)
-
+    print(f"[bench] {name}: warmup done", file=sys.stderr, flush=True)
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
            for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -175,13 +317,11 @@ def main():
         step(evs[s])
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t0) * 1e3
-    per_stage = {name: [] for name, _ in stages}
-    for s in range(args.steps):
-        for i, (name, _) in enumerate(stages):
-            per_stage[name].append(evs[s][i].elapsed_time(evs[s][i + 1]))
+    per_stage = {nm: [evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(args.steps)]
+                 for i, (nm, _) in enumerate(stages)}
     med = {n: float(np.median(v)) for n, v in per_stage.items()}
     mean = {n: float(np.mean(v)) for n, v in per_stage.items()}
-    print("[bench] timed steps done", file=sys.stderr, flush=True)
+    print(f"[bench] {name}: timed steps done", file=sys.stderr, flush=True)
     if args.copy_mib > 0:
         src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -189,98 +329,78 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # ---------------------------------------------------------- algorithmic work
-    C = causal_pairs(S)
-    idx_b = buf_b.idx.cpu().numpy()
-    idx_q = buf_q.idx.cpu().numpy()
-    idx_o = buf_o.idx.cpu().numpy()
-    elt = 2  # bf16
-
-    def sparse_bytes(idx_np, b):
-        rows = int((idx_np >= 0).sum())            # gathered support rows (per block or query)
-        gather = rows * Hkv * 2 * d * elt            # K and V rows of every KV head
-        qo = 2 * S * Hq * d * elt
-        return gather + qo + idx_np.size * 4
-
-    def sparse_flops(idx_np, b):
-        return 4 * d * Hq * causal_support_pairs(idx_np, S, b)
-
-    R_b = pb.num_blocks
-    lens_b = np.array([min(r * 64 + 64, S) for r in range(R_b)])
-    work = {
-        "frontend.project": ("hbm", 2.0 * S * D_MODEL * 2 * di,
-                             2.0 * (S * D_MODEL + 2 * di * D_MODEL + 2 * S * di) + 8.0 * di),
-        "block64.indexer_scores": ("mfma", 2.0 * di * C, None),
-        "block64.topk": ("hbm", None, 4.0 * lens_b.sum() + 4.0 * R_b * k),
-        "block64.sparse_attn": ("hbm", sparse_flops(idx_b, 64), sparse_bytes(idx_b, 64)),
-        "block64.sparse_attn_paged": ("hbm", sparse_flops(idx_b, 64), sparse_bytes(idx_b, 64)),
-        "perquery.indexer_scores": ("hbm", 2.0 * di * C, 4.0 * C + 2.0 * S * di * elt),
-        "perquery.topk": ("hbm", None, 4.0 * C + 4.0 * S * k),
-        "perquery.sparse_attn": ("hbm", sparse_flops(idx_q, 1), sparse_bytes(idx_q, 1)),
-        # algorithmic work of one scoring of every causal pair (the passes
-        # recompute it; that is overhead, not work)
-        "perquery.fused_scores_topk": ("mfma", 2.0 * di * C, 2.0 * S * di * elt + 4.0 * S * k),
-        "dense.attn": ("mfma", 4.0 * d * Hq * C, None),
-        "oracle.normalisers": ("mfma", 2.0 * d * Hq * C, None),
-        "oracle.mass": ("mfma", 2.0 * d * Hq * C, 4.0 * C),
-        "oracle.topk": ("hbm", None, 4.0 * C + 4.0 * S * k),
-        "oracle.sparse_attn": ("hbm", sparse_flops(idx_o, 1), sparse_bytes(idx_o, 1)),
-        # read P and z on s <= t, write the full gradient rows
-        "kl.loss": ("hbm", None, 2 * 4.0 * C + 4.0 * S * S + 8.0 * S),
-    }
+    elt = 2 if w.dtype == "bf16" else 4
+    work, counts = work_model(plan, S, Hq, Hkv, d, di, k, elt)
+    headline = name == "headline_32k"
     kernels = {}
-    for name, (bound, flops, nbytes) in work.items():
-        ms = mean[name]
-        ent = {"ms_median": round(med[name], 4), "ms_mean": round(ms, 4), "bound": bound}
+    for st, (bound, flops, nbytes) in work.items():
+        ms = mean[st]
+        ent = {"ms_median": round(med[st], 4), "ms_mean": round(ms, 4), "bound": bound}
         if flops is not None:
             ent["tflops"] = round(flops / (ms * 1e-3) / 1e12, 2)
-            ent["frac_mfma_bf16"] = round(ent["tflops"] / BF16_PEAK_TFLOPS, 4)
+            if elt == 2:
+                ent["frac_mfma_bf16"] = round(ent["tflops"] / BF16_PEAK_TFLOPS, 4)
+            else:
+                ent["frac_valu_fp32"] = round(ent["tflops"] / FP32_VALU_PEAK_TFLOPS, 4)
         if nbytes is not None:
             ent["gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
-            ent["frac_hbm"] = round(ent["gbs"] / HBM_PEAK_GBS, 4)
-        tb = stage_traffic(TRAFFIC_SUMMARY, name)
-        if tb is not None:
-            # DRAM bytes from the counters: kernels whose gathers hit in L2 or the
-            # Infinity Cache move far fewer bytes than the algorithmic count
-            ent["traffic_gb"] = round(tb / 1e9, 3)
-            ent["dram_gbs"] = round(tb / (ms * 1e-3) / 1e9, 1)
-            ent["frac_dram"] = round(ent["dram_gbs"] / HBM_PEAK_GBS, 4)
-        kernels[name] = ent
+            if ent["gbs"] <= HBM_PEAK_GBS:
+                ent["frac_hbm"] = round(ent["gbs"] / HBM_PEAK_GBS, 4)
+            else:
+                # gathered rows served from L2 and the Infinity Cache: the
+                # algorithmic byte rate is a gather rate, not an HBM fraction
+                ent["gather_gbs_above_hbm_peak"] = True
+        if headline:
+            tb = stage_traffic(TRAFFIC_SUMMARY, st)
+            if tb is not None:
+                # DRAM bytes from the counters
+                ent["traffic_gb"] = round(tb / 1e9, 3)
+                ent["dram_gbs"] = round(tb / (ms * 1e-3) / 1e9, 1)
+                ent["frac_dram"] = round(ent["dram_gbs"] / HBM_PEAK_GBS, 4)
+            mc = stage_counters(MFMA_SUMMARY, st)
+            if mc is not None:
+                # matrix-core busy cycles per SIMD over the launch, from the
+                # committed counter run: at the running clock, and at the
+                # published peak's 2.4 GHz
+                ent["mfma_busy"] = round(mc["mfma_busy"], 4)
+                ent["mfma_busy_vs_2p4ghz"] = round(mc["mfma_busy_peak"], 4)
+                ent["clock_ghz"] = round(mc["clock_ghz"], 3)
+        kernels[st] = ent
 
-    block_ms = sum(med[n] for n in ("block64.indexer_scores", "block64.topk", "block64.sparse_attn"))
-    pq_ms = sum(med[n] for n in ("perquery.indexer_scores", "perquery.topk", "perquery.sparse_attn"))
-    pqf_ms = med["perquery.fused_scores_topk"] + med["perquery.sparse_attn"]
-    or_ms = sum(med[n] for n in ("oracle.normalisers", "oracle.mass", "oracle.topk",
-                                 "oracle.sparse_attn"))
-    dense_ms = med["dense.attn"]
-
-    # the roofline object covers the dominant kernel of the headline path (the
-    # block-shared indexer mode that `value` times)
-    headline = ("block64.indexer_scores", "block64.topk", "block64.sparse_attn")
-    dom = max(headline, key=lambda n: mean[n])
+    modes = {m: round(sum(med[s] for s in sts), 4) for m, sts in plan.modes.items()}
+    value_ms = modes[plan.value_mode]
+    dense_ms = modes["dense"]
+    # roofline of the dominant kernel of the measured mode
+    dom = max(plan.modes[plan.value_mode], key=lambda n: mean[n])
     bound, flops, nbytes = work[dom]
     ms_dom = mean[dom]
     if bound == "mfma":
         roof = {"bound": "mfma", "achieved": round(flops / (ms_dom * 1e-3) / 1e12, 2),
                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+    elif bound == "alu":
+        roof = {"bound": "alu", "achieved": round(flops / (ms_dom * 1e-3) / 1e12, 3),
+                "peak": FP32_VALU_PEAK_TFLOPS, "unit": "TFLOP/s"}
     else:
         roof = {"bound": "hbm", "achieved": round(nbytes / (ms_dom * 1e-3) / 1e9, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     # HBM bytes per launch from the committed rocprofv3 counter runs, only while
     # the kernel's sources are unchanged since they were taken
-    roof["traffic"] = stage_traffic(TRAFFIC_SUMMARY, dom)
+    roof["traffic"] = stage_traffic(TRAFFIC_SUMMARY, dom) if headline else None
     roof["kernel"] = dom
     roof["launch_ms"] = round(ms_dom, 4)
 
-    # ------------------------------------------------------------- CPU baseline
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(inp, S, Hq, d, k, args.cpu_units)
+        cpu = cpu_baseline(plan, inp, counts, args.cpu_seconds)
 
+    b_val = plan.tables[plan.value_mode][1] if plan.value_mode in plan.tables else 1
+    cfg = {"workload": w.name, "seq_len": S, "num_q_heads": Hq, "num_kv_heads": Hkv,
+           "head_dim": d, "index_dim": di, "topk": k, "block_q": b_val,
+           "local_window": w.local_window, "selection": plan.value_mode}
     out = {
-        "metric": "ms/layer sparse GQA prefill @32K, speedup vs own dense, % HBM/MFMA roofline",
-        "value": round(block_ms, 4),
+        "metric": METRIC,
+        "value": value_ms,
         "unit": "ms/layer",
         "n_gpus": 1,
         "steps": args.steps,
@@ -289,56 +409,146 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": w.dtype,
         "data": "synthetic (seeded Gaussian Q/K/V and indexer vectors, planted needles)",
-        "config": {"workload": w.name, "seq_len": S, "num_q_heads": Hq, "num_kv_heads": Hkv,
-                   "head_dim": d, "index_dim": di, "topk": k, "block_q": 64,
-                   "selection": "indexer, 64-query blocks, max aggregation"},
-        "speedup_vs_dense": round(dense_ms / block_ms, 3),
-        "dense_ms": round(dense_ms, 4),
-        "per_query_ms_per_layer": round(pq_ms, 4),
-        "per_query_speedup_vs_dense": round(dense_ms / pq_ms, 3),
-        "per_query_fused_ms_per_layer": round(pqf_ms, 4),
-        "oracle_mode_ms_per_layer": round(or_ms, 4),
+        "config": cfg,
+        "speedup_vs_dense": round(dense_ms / value_ms, 3),
+        "dense_ms": dense_ms,
+        "modes_ms_per_layer": modes,
+        "mode_speedups_vs_dense": {m: round(dense_ms / v, 3) for m, v in modes.items()
+                                   if m != "dense"},
         "roofline": roof,
         "kernels": kernels,
         "cpu_baseline": cpu,
         "paper_context": {"ttft_speedup_npu_qwen3.5_0.8b_256k": 1.71,
                           "ttft_speedup_gpu80g_qwen3.5_9b_256k": 1.93},
     }
+    if headline:
+        # names kept from earlier bench lines
+        out["per_query_ms_per_layer"] = modes["perquery"]
+        out["per_query_speedup_vs_dense"] = round(dense_ms / modes["perquery"], 3)
+        out["per_query_fused_ms_per_layer"] = modes["perquery_fused"]
+        out["oracle_mode_ms_per_layer"] = modes["oracle"]
     print(json.dumps(out), flush=True)
+    del plan, dev, inp
+    torch.cuda.empty_cache()
 
 
-def cpu_baseline(inp, S, Hq, d, k, n_units):
-    """The fp64 oracle on the host, timed on a bounded sample of selection blocks.
+def cpu_model() -> str:
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
-    It runs the same three stages as `value` (indexer scores with 64-query
-    max aggregation, top-k, restricted attention) for n_units blocks spread
-    evenly over the sequence, and scales the time to the whole layer by the
-    causal length of each block (the work of every stage grows with it).
+
+def _spread(n_total, n, include=()):
+    return np.unique(np.concatenate([np.linspace(0, n_total - 1, n).round().astype(int),
+                                     np.asarray(include, dtype=int)]))
+
+
+def cpu_baseline(plan, inp, counts, seconds):
+    """The fp64 oracle on the host, timed on bounded samples of the workload.
+
+    Legs: the measured mode (indexer scores, top-k, restricted attention, or
+    the oracle mode for the tiny workload), dense attention, and oracle mode
+    where the workload runs it. Each stage runs on evenly spaced selection
+    blocks (query rows for dense), and its time is scaled to the whole layer
+    by that stage's own work: causal length for scoring, mass and top-k,
+    causal pairs for dense, and kept (query, key) pairs for restricted
+    attention (counted on the GPU's support tables, which hold the same
+    number of pairs per block as a correct selection).
     """
     import oracle
-    b = 64
-    R = (S + b - 1) // b
-    units = np.unique(np.linspace(0, R - 1, n_units).round().astype(int))
+    w = plan.w
+    S, k = w.seq_len, w.topk
     q64, k64, v64 = oracle._f64(inp.q), oracle._f64(inp.k), oracle._f64(inp.v)
-    qi, ki = oracle._f64(inp.q_idx), oracle._f64(inp.k_idx)
     oracle._load()
-    t0 = time.perf_counter()
-    Y = oracle.support_scores("indexer", units, b, q_idx=qi, k_idx=ki, agg="max")
-    sel = oracle.select(Y, units, b, S, k)
-    table = np.full((R, k), -1, dtype=np.int32)
-    table[units] = sel
-    rows = np.concatenate([np.arange(u * b, min(u * b + b, S)) for u in units])
-    oracle.sparse(q64, k64, v64, table, b, rows=rows)
-    secs = time.perf_counter() - t0
-    L = np.array([min(r * b + b, S) for r in range(R)], dtype=np.float64)
-    scale = L.sum() / L[units].sum()
-    ms_layer = secs * scale * 1e3
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": round(ms_layer, 1), "unit": "ms/layer", "cores": cores, "kind": "oracle",
-            "sample": f"{len(units)} of {R} 64-query blocks (indexer scores, top-k, sparse "
-                      f"attention), {secs:.1f}s measured, scaled by causal length"}
+    legs = {}
+
+    def timed(fn):
+        t0 = time.perf_counter()
+        r = fn()
+        return r, time.perf_counter() - t0
+
+    def selection_leg(mode, prefix, b, agg="max", W=0, qi=None, ki=None):
+        R = (S + b - 1) // b
+        L = np.minimum(np.arange(R) * b + b, S).astype(np.float64)
+        # sample size: aim for about `seconds` of CPU time (flops per block
+        # of scoring and restricted attention at a planning rate)
+        hd = w.head_dim * w.num_q_heads
+        score = 2 * w.index_dim if mode == "indexer" else 4 * hd
+        per_unit = b * (L.mean() * score + 4 * min(k, L.mean()) * hd) / CPU_PLAN_FLOPS
+        n = int(max(4, min(R, seconds / max(per_unit, 1e-9))))
+        units = _spread(R, n)
+        if mode == "indexer":
+            Y, t_sc = timed(lambda: oracle.support_scores("indexer", units, b, q_idx=qi, k_idx=ki,
+                                                          agg=agg))
+        else:
+            Y, t_sc = timed(lambda: oracle.support_scores("oracle", units, b, q=q64, k=k64))
+        sel, t_tk = timed(lambda: oracle.select(Y, units, b, S, k, W))
+        table = np.full((R, k), -1, dtype=np.int32)
+        table[units] = sel
+        rows = np.concatenate([np.arange(u * b, min(u * b + b, S)) for u in units])
+        _, t_sp = timed(lambda: oracle.sparse(q64, k64, v64, table, b, rows=rows))
+        # kept pairs of the sampled blocks under the oracle's own selection
+        pairs_s = 0
+        for u in units:
+            srt = np.sort(table[u][table[u] >= 0])
+            ts = np.arange(u * b, min(u * b + b, S))
+            pairs_s += int(np.searchsorted(srt, ts, side="right").sum())
+        pairs_all = counts[prefix][1].sum() if prefix in counts else pairs_s * R / len(units)
+        scale_L = L.sum() / L[units].sum()
+        ms = 1e3 * ((t_sc + t_tk) * scale_L + t_sp * pairs_all / max(pairs_s, 1))
+        legs[prefix] = {"ms_per_layer": round(ms, 1),
+                        "sample": f"{len(units)} of {R} {b}-query blocks",
+                        "measured_s": round(t_sc + t_tk + t_sp, 2)}
+        return ms
+
+    def dense_leg():
+        per_row = 4.0 * S / 2 * w.head_dim * w.num_q_heads / CPU_PLAN_FLOPS
+        n = int(max(4, min(S, seconds / max(per_row, 1e-9))))
+        rows = _spread(S, n, include=[S - 1])
+        _, t = timed(lambda: oracle.dense(q64, k64, v64, rows=rows))
+        scale = (S * (S + 1) / 2) / float((rows + 1).sum())
+        legs["dense"] = {"ms_per_layer": round(1e3 * t * scale, 1),
+                         "sample": f"{len(rows)} of {S} query rows", "measured_s": round(t, 2)}
+
+    vm = plan.value_mode
+    if vm == "oracle":
+        selection_leg("oracle", "oracle", 1)
+    else:
+        buf, b = plan.tables[vm]
+        agg = "sum" if vm.endswith("sum") else "max"
+        if vm.startswith("untrained"):
+            qi, ki = (oracle._f64(t) for t in plan.extra["untrained"])
+        else:
+            qi, ki = oracle._f64(inp.q_idx), oracle._f64(inp.k_idx)
+        W = w.local_window if vm.startswith("block64") and w.name == "block_16k" else 0
+        selection_leg("indexer", vm, b, agg=agg, W=W, qi=qi, ki=ki)
+        if "oracle" in plan.modes:
+            selection_leg("oracle", "oracle", 1)
+    dense_leg()
+    main = legs[vm]
+    return {"value": main["ms_per_layer"], "unit": "ms/layer", "cores": oracle.num_threads(),
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "sample": f"{main['sample']} ({vm} mode), {main['measured_s']} s measured, each "
+                      "stage scaled by its own work (causal length for scores and top-k, "
+                      "kept pairs for restricted attention)",
+            "legs": legs}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the path shards by selection blocks, see the design notes)", file=sys.stderr)
+        sys.exit(2)
+    names = ALL_WORKLOADS if args.workload == "all" else (args.workload,)
+    for n in names:
+        run_workload(args, n)
 
 
 if __name__ == "__main__":

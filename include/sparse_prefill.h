@@ -39,8 +39,11 @@
  *
  * Memory and ownership: every pointer is a DEVICE pointer allocated and
  * owned by the caller, 16-byte aligned, and inputs never alias outputs.
- * The library allocates nothing and keeps no mutable global state apart
- * from a per-device cache of the device architecture.
+ * The library allocates nothing. Its only mutable global state is a set of
+ * per-device caches filled on first use and never invalidated: the device
+ * architecture, the compute-unit count, and the resident-workgroup count
+ * of each persistent kernel instance (all written atomically, so calls from
+ * several host threads are safe).
  *
  * Execution: each call validates its arguments on the host before any HIP
  * call (so validation needs no GPU), then enqueues its kernels on `stream`
@@ -103,7 +106,8 @@ typedef struct sp_problem {
   int32_t agg;          /* SP_AGG_MAX (Section 4.2) or SP_AGG_SUM */
   int32_t relu;         /* 1: ReLU on indexer scores (Section 6.3); 0: raw */
   int32_t dtype;        /* SP_DTYPE_F32 or SP_DTYPE_BF16 for q,k,v,o,q_idx,k_idx */
-  float attn_scale;     /* 0 => 1/sqrt(d) (Section 3) */
+  float attn_scale;     /* 0 => 1/sqrt(d) (Section 3); otherwise finite and
+                           positive: a negative value is SP_ERR_SHAPE */
   float index_scale;    /* 0 => 1/sqrt(d_idx) (Section 6.3) */
   int32_t head_axis;    /* support granularity on the head axis (Section 3):
                            0: one head-averaged token support S_t shared by all

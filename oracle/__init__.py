@@ -31,6 +31,9 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "sp_oracle.c")
 _LIB = os.path.join(_HERE, "libsp_oracle.so")
+# A prebuilt copy of the same source to load instead (the sanitizer test
+# builds one with AddressSanitizer and UBSan); it is used as it is.
+_LIB_OVERRIDE = os.environ.get("SP_ORACLE_LIB")
 _lib = None
 
 AGG = {"max": 0, "sum": 1}
@@ -49,9 +52,12 @@ def build(force: bool = True) -> str:
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-            build(force=True)
-        lib = ctypes.CDLL(_LIB)
+        if _LIB_OVERRIDE:
+            lib = ctypes.CDLL(_LIB_OVERRIDE)
+        else:
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build(force=True)
+            lib = ctypes.CDLL(_LIB)
         P = ctypes.c_void_p
         I = ctypes.c_int
         D = ctypes.c_double
@@ -64,11 +70,18 @@ def _load():
         lib.orc_mass_heads.argtypes = [I, I, I, I, D, P, P, I, I, I, P, P]
         lib.orc_kl.argtypes = [I, I, P, P, P, P, P]
         lib.orc_project.argtypes = [I, I, I, P, P, P, P, P, D, D, I, I, P, P, P]
+        lib.orc_num_threads.argtypes = []
+        lib.orc_num_threads.restype = ctypes.c_int
         for f in ("orc_dense", "orc_mass", "orc_index_scores", "orc_block_aggregate",
                   "orc_topk", "orc_sparse", "orc_kl", "orc_project", "orc_mass_heads"):
             getattr(lib, f).restype = None
         _lib = lib
     return _lib
+
+
+def num_threads() -> int:
+    """Threads the oracle's OpenMP loops use on this host."""
+    return int(_load().orc_num_threads())
 
 
 def _f64(a) -> np.ndarray:

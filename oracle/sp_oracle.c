@@ -16,6 +16,7 @@
  * Layouts: q [S,Hq,d], k and v [S,Hkv,d], q_idx and k_idx [S,d_idx].
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -369,3 +370,6 @@ void orc_project(int S, int dm, int di, const double *x, const double *wq, const
     free(b);
   }
 }
+
+/* Threads the parallel loops above run on (reported beside CPU timings). */
+int orc_num_threads(void) { return omp_get_max_threads(); }

@@ -29,6 +29,9 @@ int check_common(const sp_problem *p) {
   if (p->causal != 1) return SP_ERR_UNSUPPORTED;
   if (p->dtype != SP_DTYPE_F32 && p->dtype != SP_DTYPE_BF16) return SP_ERR_UNSUPPORTED;
   if (!isfinite(p->attn_scale) || !isfinite(p->index_scale)) return SP_ERR_SHAPE;
+  // The attention kernels take row maxima of raw scores and scale them
+  // afterwards, which needs scale >= 0 (the paper's 1/sqrt(d) is positive).
+  if (p->attn_scale < 0.f) return SP_ERR_SHAPE;
   return SP_OK;
 }
 
@@ -67,10 +70,12 @@ Prob resolve(const sp_problem *p) {
   r.d = p->head_dim;
   r.di = p->index_dim;
   r.k = p->topk;
-  r.b = p->block_q < 1 ? 1 : p->block_q;
   r.qo = p->q_offset;
   r.nq = r.S - r.qo;
-  r.R = (r.nq + r.b - 1) / r.b;
+  // a block longer than the call's rows is one block of all of them (same
+  // result, and no kernel forms b * G or t0 + b beyond int range)
+  r.b = p->block_q < 1 ? 1 : p->block_q < r.nq ? p->block_q : r.nq;
+  r.R = r.nq / r.b + (r.nq % r.b != 0);
   r.W = p->local_window;
   r.agg = p->agg;
   r.relu = p->relu;

@@ -25,13 +25,13 @@
 #include "common.hpp"
 #include "kernels.hpp"
 #include "mfma.hpp"
+#include "persistent_units.hpp"
 
 namespace sp {
 namespace {
 
 constexpr int kQW = 64;     // queries per wave
 constexpr int kKC = 1024;   // keys per workgroup chunk (rows kernel)
-constexpr int kXcds = 8;    // XCDs of the chip; workgroup i runs on XCD i % 8
 constexpr int kIdxBufferDword3 = 0x00020000;   // raw buffer resource: 32-bit data format
 // Waits until this wave's vector memory operations (direct-to-LDS key tile
 // loads and stores) have completed; LDS and scalar counters are not checked.
@@ -84,49 +84,8 @@ __device__ __forceinline__ uint32_t as_u(float x) { return __float_as_uint(x); }
 // MAXPOS: aggregation is max and the scale is non-negative, so scale and
 // ReLU commute with the max: rows are reduced on raw MFMA outputs and only
 // the reduced value is scaled; tiles entirely below a wave's first query
-// skip the causal test.
-// Work of the block kernel is the sequence of units (query group qg, key
-// tile t) for t < tiles(qg), ordered by group, then tile; tiles(qg) counts
-// the key tiles at or below the group's last query (causal, Section 4.2).
-// The grid is persistent, as many workgroups as fit on the chip at once, and
-// splits the sequence into equal contiguous runs: every CU gets the same
-// number of key tiles (to one) whatever the causal shape, key tiles stream
-// through one pipeline across unit boundaries, and query operands are
-// reloaded only where a run enters a new group. Workgroup i (which the
-// hardware places on XCD i % 8) takes run (i % 8) * n/8 + i / 8 (remainder
-// spread over the first XCDs), so each XCD's L2 sees a contiguous range of
-// groups and the key tiles they share.
-// g0: first query group (a chunked call starting at g0 * QG covers groups
-// g0 ..).
-template <int QG, int KT>
-struct UnitCursor {
-  int S, qg, t, nt;   // sequence length, current group, tile, tiles of the group
-  __host__ __device__ static int tiles(int S, int g) {
-    return (min((g + 1) * QG, S) + KT - 1) / KT;
-  }
-  __device__ void seek(int g0, long long u) {
-    qg = g0;
-    for (;;) {
-      nt = tiles(S, qg);
-      if (u < nt) break;
-      u -= nt;
-      ++qg;
-    }
-    t = (int)u;
-  }
-};
-
-__device__ __forceinline__ int xcd_run(int i, int n) {
-  const int x = i % kXcds, j = i / kXcds;
-  return x * (n / kXcds) + min(x, n % kXcds) + j;
-}
-
-template <int QG, int KT>
-long long count_units(int S, int g0) {
-  long long n = 0;
-  for (int g = g0; g * QG < S; ++g) n += UnitCursor<QG, KT>::tiles(S, g);
-  return n;
-}
+// skip the causal test. The kernel's split of (query group, key tile) units
+// over its persistent grid is in persistent_units.hpp.
 
 // Key tiles of the block kernel: NSUB sub-tiles of 64 keys, staged one tile
 // ahead through registers into double-buffered LDS.
@@ -232,8 +191,8 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 31, h = lane >> 5;
   const int run = xcd_run(blockIdx.x, gridDim.x);
-  const int u0 = (int)((long long)n_units * run / gridDim.x);
-  const int u1 = (int)((long long)n_units * (run + 1) / gridDim.x);
+  int u0, u1;
+  run_units(n_units, run, gridDim.x, u0, u1);
   if (u0 == u1) return;
   UnitCursor<QG, KT> uc;
   uc.S = S;
@@ -554,9 +513,7 @@ __global__ __launch_bounds__(NW * 64) void indexer_block_kernel(int S, int g0, i
       wait_vmem();
       __syncthreads();
     }
-    uc.qg = group + 1;
-    uc.t = 0;
-    uc.nt = UnitCursor<QG, KT>::tiles(S, group + 1);
+    uc.next_group();
   }
   if constexpr (BQ <= kQW) {
     if constexpr (DI <= 128)
@@ -650,35 +607,41 @@ __global__ __launch_bounds__(256) void indexer_rows_kernel(int S, int qo, int re
   }
 }
 
-// Launches `kernel` as a persistent grid: as many workgroups as are resident
-// on the current device at once (CUs times the kernel's occupancy, both
-// cached per device), at most one per unit of work.
-template <class... KArgs, class... Args>
-hipError_t launch_persistent(void (*kernel)(KArgs...), int threads, int n_units,
-                             hipStream_t st, Args... args) {
-  constexpr int kMaxDevices = 64;
-  static std::atomic<int> per_cu{0};
-  static std::atomic<int> cus[kMaxDevices];
+// Per-device caches of the persistent launch: compute units per device, and
+// resident workgroups per CU for each kernel instance K (instances differ in
+// LDS and registers, so each has its own entry).
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cus[kMaxDevices];
+template <auto K>
+struct Residency {
+  static inline std::atomic<int> per_cu[kMaxDevices];
+};
+
+// Launches kernel K as a persistent grid: as many workgroups as are resident
+// on the current device at once (CUs times K's occupancy), at most one per
+// unit of work.
+template <auto K, class... Args>
+hipError_t launch_persistent(int threads, int n_units, hipStream_t st, Args... args) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-  int c = cus[dev].load(std::memory_order_relaxed);
+  int c = g_cus[dev].load(std::memory_order_relaxed);
   if (c == 0) {
     e = hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
-    cus[dev].store(c, std::memory_order_relaxed);
+    g_cus[dev].store(c, std::memory_order_relaxed);
   }
-  int w = per_cu.load(std::memory_order_relaxed);
+  int w = Residency<K>::per_cu[dev].load(std::memory_order_relaxed);
   if (w == 0) {
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&w, kernel, threads, 0);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&w, K, threads, 0);
     if (e != hipSuccess) return e;
     w = w < 1 ? 1 : w;
-    per_cu.store(w, std::memory_order_relaxed);
+    Residency<K>::per_cu[dev].store(w, std::memory_order_relaxed);
   }
   const int grid = n_units < c * w ? n_units : c * w;
   if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL(kernel, dim3(grid), dim3(threads), 0, st, args...);
+  hipLaunchKernelGGL(K, dim3(grid), dim3(threads), 0, st, args...);
   return hipGetLastError();
 }
 
@@ -709,11 +672,11 @@ hipError_t launch_di(const Prob &p, const void *qi, const void *ki, float *score
   const bool maxpos = p.agg == SP_AGG_MAX && p.iscale >= 0.f;
 #define SP_BLK(BQ)                                                                           \
   if (maxpos)                                                                                \
-    err = launch_persistent(indexer_block_kernel<DI, BQ, true, NW>, NW * 64, n_units, st, p.S, \
-                            g0, n_units, p.agg, p.relu, p.iscale, q, k, y);                  \
+    err = launch_persistent<indexer_block_kernel<DI, BQ, true, NW>>(                         \
+        NW * 64, n_units, st, p.S, g0, n_units, p.agg, p.relu, p.iscale, q, k, y);           \
   else                                                                                       \
-    err = launch_persistent(indexer_block_kernel<DI, BQ, false, NW>, NW * 64, n_units, st,   \
-                            p.S, g0, n_units, p.agg, p.relu, p.iscale, q, k, y)
+    err = launch_persistent<indexer_block_kernel<DI, BQ, false, NW>>(                        \
+        NW * 64, n_units, st, p.S, g0, n_units, p.agg, p.relu, p.iscale, q, k, y)
   hipError_t err;
   switch (p.b) {
     case 16: SP_BLK(16); break;

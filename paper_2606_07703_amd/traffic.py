@@ -187,15 +187,137 @@ def stage_traffic(path: str, stage: str) -> Optional[float]:
     return e["bytes"] if e and e["current"] else None
 
 
+# ------------------------------------------------------- matrix-core counters
+# gfx950: 256 CUs of 4 SIMDs; GRBM counters are summed over the 8 XCDs.
+N_SIMD = 1024
+N_XCD = 8
+PUBLISHED_CLOCK_GHZ = 2.4
+MFMA_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CYCLES", "GRBM_GUI_ACTIVE")
+
+
+def read_dispatch_counters(run_dir: str) -> List[Dict]:
+    """[{id, name, ns, counters{name: value}}] in dispatch order."""
+    paths = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not paths:
+        raise FileNotFoundError(f"no counter_collection.csv under {run_dir}")
+    per: Dict[int, Dict] = {}
+    for p in paths:
+        for r in csv.DictReader(open(p)):
+            did = int(r["Dispatch_Id"])
+            e = per.setdefault(did, {"id": did, "name": r["Kernel_Name"], "counters": {},
+                                     "ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
+            c = r["Counter_Name"]
+            e["counters"][c] = e["counters"].get(c, 0.0) + float(r["Counter_Value"])
+    return [per[k] for k in sorted(per)]
+
+
+def summarize_mfma(run_dir: str) -> Dict:
+    """Per bench stage (the first dispatch of the stage's kernels, averaged
+    over steps): MFMA busy cycles per SIMD as a fraction of the launch's
+    cycles at the running shader clock (GRBM_GUI_ACTIVE per XCD over the
+    launch duration) and at the published peak's clock."""
+    ds = [d for d in read_dispatch_counters(run_dir) if LIB_KERNEL_RE.search(d["name"])]
+    per_step = sum(STAGE_DISPATCHES.get(st, 1) for st in STAGES)
+    if len(ds) % per_step:
+        raise ValueError(f"{len(ds)} library dispatches is not a whole number of "
+                         f"{per_step}-dispatch steps")
+    nsteps = len(ds) // per_step
+    out = {"stages": {}}
+    first = 0
+    for st in STAGES:
+        nd = STAGE_DISPATCHES.get(st, 1)
+        busy = cyc = ns = sqb = 0.0
+        for s in range(nsteps):
+            for x in range(nd):
+                d = ds[s * per_step + first + x]
+                busy += d["counters"].get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+                cyc += d["counters"].get("GRBM_GUI_ACTIVE", 0.0) / N_XCD
+                sqb += d["counters"].get("SQ_BUSY_CYCLES", 0.0)
+                ns += d["ns"]
+        files = kernel_sources(STAGE_KERNEL_FILE[st])
+        out["stages"][st] = {
+            "kernel": _short(ds[first]["name"]),
+            "ms": ns / nsteps / 1e6,
+            "clock_ghz": cyc / ns,
+            "mfma_busy": busy / (N_SIMD * cyc) if cyc else 0.0,
+            "mfma_busy_peak": busy / (N_SIMD * PUBLISHED_CLOCK_GHZ * ns) if ns else 0.0,
+            "se_busy": sqb / (32 * cyc) if cyc else 0.0,
+            "mfma_busy_cycles": busy / nsteps,
+            "sources": files,
+            "digest": sources_digest(files),
+        }
+        first += nd
+    return out
+
+
+def write_mfma_md(path: str, s: Dict, cmd: str, parse_cmd: str) -> None:
+    L = ["# Matrix-core utilisation per launch: headline 32K workload, every bench stage", "",
+         "One rocprofv3 counter run of one bench step. Per launch: SQ_VALU_MFMA_BUSY_CYCLES",
+         f"(summed over the {N_SIMD} SIMDs), GRBM_GUI_ACTIVE (summed over the {N_XCD} XCDs) "
+         "and SQ_BUSY_CYCLES",
+         "(summed over the 32 shader engines), with the launch duration from the trace.", "",
+         "* clock = GRBM_GUI_ACTIVE / 8 / duration (the shader clock under this load);",
+         f"* MFMA busy = MFMA busy cycles / ({N_SIMD} x GRBM_GUI_ACTIVE / 8): the share of the "
+         "launch's cycles the matrix cores are busy, at the running clock;",
+         f"* vs peak = MFMA busy cycles / ({N_SIMD} x {PUBLISHED_CLOCK_GHZ} GHz x duration): "
+         "the same against the published 2.5 PFLOP/s bf16 peak's clock;",
+         "* SE busy = SQ_BUSY_CYCLES / (32 x GRBM_GUI_ACTIVE / 8): cycles in which a shader "
+         "engine holds any wave.", "",
+         "A 32x32x16 bf16 MFMA keeps a SIMD's matrix core busy 32 cycles (1024 FLOP per busy "
+         "cycle).", "",
+         "Commands (repository root, one MI355X):", "", "    " + cmd, "    " + parse_cmd, "",
+         "| stage | kernel | ms | clock GHz | MFMA busy | vs peak | SE busy | digest |",
+         "|---|---|---:|---:|---:|---:|---:|---|"]
+    for st in STAGES:
+        e = s["stages"][st]
+        L.append(f"| {st} | `{e['kernel']}` | {e['ms']:.4f} | {e['clock_ghz']:.3f} | "
+                 f"{100 * e['mfma_busy']:.1f}% | {100 * e['mfma_busy_peak']:.1f}% | "
+                 f"{100 * e['se_busy']:.1f}% | {e['digest']} |")
+    L += ["", "<!-- machine-readable: stage mfma_busy mfma_busy_peak clock_ghz digest -->"]
+    for st in STAGES:
+        e = s["stages"][st]
+        L.append(f"<!-- mfma {st} {e['mfma_busy']:.6f} {e['mfma_busy_peak']:.6f} "
+                 f"{e['clock_ghz']:.6f} {e['digest']} -->")
+    open(path, "w").write("\n".join(L) + "\n")
+
+
+def stage_counters(path: str, stage: str) -> Optional[Dict]:
+    """{mfma_busy, mfma_busy_peak, clock_ghz} of a stage from a summary file,
+    while the digest of the kernel's sources still matches the tree."""
+    if not os.path.exists(path):
+        return None
+    for m in re.finditer(r"<!-- mfma (\S+) (\S+) (\S+) (\S+) (\S+) -->", open(path).read()):
+        if m.group(1) != stage or stage not in STAGE_KERNEL_FILE:
+            continue
+        if sources_digest(kernel_sources(STAGE_KERNEL_FILE[stage])) != m.group(5):
+            return None
+        return {"mfma_busy": float(m.group(2)), "mfma_busy_peak": float(m.group(3)),
+                "clock_ghz": float(m.group(4))}
+    return None
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
-    ap.add_argument("--fetch", required=True, help="rocprofv3 output dir of the FETCH_SIZE run")
-    ap.add_argument("--write", required=True, help="rocprofv3 output dir of the WRITE_SIZE run")
-    ap.add_argument("--copy-mib", type=int, required=True)
+    ap.add_argument("--fetch", help="rocprofv3 output dir of the FETCH_SIZE run")
+    ap.add_argument("--write", help="rocprofv3 output dir of the WRITE_SIZE run")
+    ap.add_argument("--copy-mib", type=int)
     ap.add_argument("--out", required=True)
-    ap.add_argument("--cmd-fetch", required=True)
-    ap.add_argument("--cmd-write", required=True)
+    ap.add_argument("--cmd-fetch")
+    ap.add_argument("--cmd-write")
+    ap.add_argument("--mfma", help="rocprofv3 output dir of the matrix-core counter run "
+                                   "(writes the utilisation summary instead)")
+    ap.add_argument("--cmd-mfma")
     a = ap.parse_args(argv)
+    if a.mfma:
+        s = summarize_mfma(a.mfma)
+        parse_cmd = (f"python3 -m paper_2606_07703_amd.traffic --mfma {a.mfma} --out {a.out} "
+                     "--cmd-mfma '...'")
+        write_mfma_md(a.out, s, a.cmd_mfma or "", parse_cmd)
+        for st in STAGES:
+            e = s["stages"][st]
+            print(f"{st:26s} {e['ms']:8.4f} ms  MFMA busy {100 * e['mfma_busy']:5.1f}%  "
+                  f"vs peak {100 * e['mfma_busy_peak']:5.1f}%  clock {e['clock_ghz']:.3f}")
+        return
     s = summarize(a.fetch, a.write, a.copy_mib << 20)
     parse_cmd = (f"python3 -m paper_2606_07703_amd.traffic --fetch {a.fetch} --write {a.write} "
                  f"--copy-mib {a.copy_mib} --out {a.out} --cmd-fetch '...' --cmd-write '...'")

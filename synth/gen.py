@@ -14,6 +14,12 @@ Recipe (one numpy PCG64 stream per call, fixed draw order):
 4. Everything is drawn in fp32 and rounded once to the storage dtype
    (bf16 by round-to-nearest-even through torch).
 
+Two test-only shapes of the same draws: ``unit_v=True`` drops the 1/sqrt(d)
+of V (outputs of order 1/sqrt(|support|) instead of 1/sqrt(d |support|)),
+and ``k_ramp=g`` multiplies key row s by 1 + g*s/(S-1) before the needles
+are planted, so later keys carry ever larger logits and an online softmax
+must raise its running maximum long after its first tile.
+
 Needle retrieval mirrors the needle-in-a-haystack task family the paper
 evaluates on (Section 5.1); no benchmark item is reproduced.
 """
@@ -52,13 +58,18 @@ def _rng(seed: int) -> np.random.Generator:
 def make_inputs(seq_len: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
                 index_dim: int = 0, dtype: str = "bf16", needles: int = 0,
                 stratified: bool = False, seed: int = 0, peaked: bool = False,
-                untrained: bool = False) -> Inputs:
+                untrained: bool = False, unit_v: bool = False, k_ramp: float = 0.0) -> Inputs:
     S, Hq, Hkv, d, di = seq_len, num_q_heads, num_kv_heads, head_dim, index_dim
     rng = _rng(seed)
     sd = 1.0 if peaked else 1.0 / np.sqrt(d)
     q = rng.standard_normal((S, Hq, d), dtype=np.float32) * np.float32(sd)
     k = rng.standard_normal((S, Hkv, d), dtype=np.float32) * np.float32(sd)
-    v = rng.standard_normal((S, Hkv, d), dtype=np.float32) * np.float32(1.0 / np.sqrt(d))
+    v = rng.standard_normal((S, Hkv, d), dtype=np.float32)
+    if not unit_v:
+        v *= np.float32(1.0 / np.sqrt(d))
+    if k_ramp:
+        gain = 1.0 + k_ramp * np.arange(S, dtype=np.float64) / max(S - 1, 1)
+        k *= gain.astype(np.float32)[:, None, None]
     qi = ki = None
     if di > 0:
         qi = rng.standard_normal((S, di), dtype=np.float32)
@@ -111,17 +122,25 @@ def make_scores(rows: int, seq_len: int, seed: int = 0, kind: str = "gauss") -> 
 
 
 def make_support(seq_len: int, block_q: int, topk: int, seed: int = 0,
-                 shuffle: bool = False) -> torch.Tensor:
+                 shuffle: bool = False, random_rows=None) -> torch.Tensor:
     """A random support table [R, topk] int32 for exercising sparse attention alone.
 
     Row r draws min(topk, t1_r+1) distinct positions from [0, t1_r], where t1_r
     is the last query of selection block r, stores them ascending (or shuffled)
-    and pads with -1.
+    and pads with -1. With ``random_rows`` (a list of row numbers) only those
+    rows are drawn; every other row holds its m most recent positions, which
+    keeps full-size tables cheap to make where only some rows are checked.
     """
     rng = _rng(seed)
     R = (seq_len + block_q - 1) // block_q
     out = np.full((R, topk), -1, dtype=np.int32)
-    for r in range(R):
+    drawn = range(R) if random_rows is None else sorted(set(int(r) for r in random_rows))
+    if random_rows is not None:
+        t1s = np.minimum(np.arange(R) * block_q + block_q, seq_len) - 1
+        for r in range(R):
+            m = min(topk, int(t1s[r]) + 1)
+            out[r, :m] = np.arange(t1s[r] - m + 1, t1s[r] + 1, dtype=np.int32)
+    for r in drawn:
         t1 = min(r * block_q + block_q, seq_len) - 1
         m = min(topk, t1 + 1)
         sel = np.sort(rng.choice(t1 + 1, size=m, replace=False))

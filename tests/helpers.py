@@ -75,4 +75,74 @@ def max_err(a: np.ndarray, b: np.ndarray) -> float:
 
 
 def tol_for(dtype: str) -> float:
+    """The stated absolute bound on attention outputs: bf16 2e-2, fp32 1e-5."""
     return 1e-5 if dtype == "f32" else 2e-2
+
+
+def attn_bound(ref: np.ndarray, ref_abs: np.ndarray, dtype: str) -> np.ndarray:
+    """Per-element bound on |o_gpu - o| derived from the kernels' arithmetic.
+
+    o = sum_s w_s v_s with softmax weights w_s over the usable support; A =
+    sum_s w_s |v_s| is the same attention taken over |V| (``ref_abs``).
+    bf16: each unnormalised weight exp2(l_s - m) is computed in fp32 and
+    rounded once to bf16 for the P.V product (relative error <= u = 2^-8,
+    while the normaliser sums the unrounded fp32 values), products of bf16
+    operands are exact in fp32 and summed in fp32, and o is rounded once to
+    bf16 (<= u |o|). So |o_gpu - o| <= u A + u |o| + (fp32 terms of order
+    2^-24 d); the check allows twice that. fp32: no bf16 rounding anywhere;
+    the logits carry fp32 rounding of order d * 2^-24 * sum |q_c k_c| *
+    scale, which the relative terms below cover with a wide margin.
+    Unlike a flat absolute bound this scales with the outputs: an all-zero
+    or support-mean output fails it wherever the attention is not uniform.
+    """
+    if dtype == "f32":
+        return 1e-4 * ref_abs + 1e-5 * np.abs(ref) + 1e-7
+    u = 2.0 ** -8
+    return 2 * u * ref_abs + 2 * u * np.abs(ref) + 1e-6
+
+
+def check_attention(got: np.ndarray, ref: np.ndarray, ref_abs: np.ndarray, dtype: str,
+                    label: str = "", factor: float = 1.0) -> float:
+    """Asserts the stated absolute bound and the derived per-element bound
+    (``factor`` times it, e.g. 2 for two GPU results each within it); returns
+    the worst err/bound ratio. The stated bound (bf16 2e-2, fp32 1e-5) is
+    absolute for outputs up to 1 in magnitude (every workload's outputs stay
+    below 0.05) and relative above that: the unit-spread V of the sharp test
+    inputs gives outputs up to about 5, where one bf16 rounding of the output
+    alone reaches 2^-8 * 4 = 0.0156."""
+    err = np.abs(got - ref)
+    bound = factor * attn_bound(ref, ref_abs, dtype)
+    ratio = float((err / bound).max()) if err.size else 0.0
+    rel_rms = float(np.sqrt((err ** 2).mean() / max((ref ** 2).mean(), 1e-300))) if err.size \
+        else 0.0
+    say(f"  {label}max abs err {err.max() if err.size else 0:.3e}, max|ref| "
+        f"{np.abs(ref).max() if ref.size else 0:.3e}, rms err/rms ref {rel_rms:.2e}, "
+        f"worst err/bound {ratio:.3f}")
+    assert err.size == 0 or (err <= factor * tol_for(dtype) * np.maximum(1.0, np.abs(ref))).all()
+    assert ratio <= 1.0, (ratio, label)
+    return ratio
+
+
+def logit_rise(inp, idx, b, rows, tile):
+    """Largest rise, in base-2 units, of a later support tile's maximum scaled
+    logit over the first tile's, among the given query rows and every head.
+    Support tiles are the row's usable entries in table order, `tile` at a
+    time (how the MFMA kernels walk them). Shows that a case reaches the
+    online-softmax rescale after the first tile (a rise above 8)."""
+    Hq, d = inp.q.shape[1], inp.q.shape[2]
+    G = Hq // inp.k.shape[1]
+    sl2 = 1.4426950408889634 / np.sqrt(d)
+    table = idx.numpy()
+    best = -np.inf
+    for t in rows:
+        row = table[t // b]
+        use = row[(row >= 0) & (row <= t)]
+        if len(use) <= tile:
+            continue
+        qt = inp.q[int(t)].double().numpy()
+        kt = inp.k[torch.as_tensor(use, dtype=torch.long)].double().numpy()
+        for h in range(Hq):
+            lg = (kt[:, h // G] @ qt[h]) * sl2
+            tiles = [lg[i:i + tile].max() for i in range(0, len(lg), tile)]
+            best = max(best, max(tiles[1:]) - tiles[0])
+    return best

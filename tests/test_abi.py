@@ -118,6 +118,15 @@ def test_selection_errors(kw, expect):
     assert oracle_support(prob(**kw)) == expect
 
 
+@pytest.mark.parametrize("scale", [-0.088, -1e-30, float("nan"), float("inf")])
+def test_attention_scale_must_be_positive_and_finite(scale):
+    # the MFMA attention kernels take row maxima of raw scores and scale them
+    # afterwards, which only commutes with the max for a positive scale
+    p = prob(attn_scale=scale)
+    assert dense(p) == SHAPE and sparse(p) == SHAPE and oracle_support(p) == SHAPE
+    assert rc("sp_sparse_gqa_attn_paged", p, A, A2, A3, A4, 64, 4, A5, A6, None) == SHAPE
+
+
 def test_indexer_specific_errors():
     assert indexer(prob(index_dim=96)) == UNSUP
     assert indexer(prob(index_dim=0)) == UNSUP

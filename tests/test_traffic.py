@@ -74,3 +74,46 @@ def test_ragged_dispatch_count_rejected(tmp_path):
     _write_run(tmp_path / "w", "WRITE_SIZE", [1.0] * per_step, copy_kib=1.0)
     with pytest.raises(ValueError):
         T.summarize(str(tmp_path / "f"), str(tmp_path / "w"), 1 << 20)
+
+
+def _write_mfma_run(d, per_dispatch, ns=100_000):
+    """One bench step of dispatches, each with the three matrix-core counters."""
+    os.makedirs(d, exist_ok=True)
+    with open(os.path.join(d, "run_counter_collection.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Dispatch_Id", "Kernel_Name", "Counter_Name",
+                                          "Counter_Value", "Start_Timestamp", "End_Timestamp"])
+        w.writeheader()
+        t = 1_000_000
+        for i, (busy, gui) in enumerate(per_dispatch):
+            for cname, v in (("SQ_VALU_MFMA_BUSY_CYCLES", busy), ("GRBM_GUI_ACTIVE", gui),
+                             ("SQ_BUSY_CYCLES", 32 * gui / 8)):
+                for part in (v / 2, v / 2):   # two instances, summed
+                    w.writerow({"Dispatch_Id": i + 1, "Kernel_Name":
+                                f"void sp::(anonymous namespace)::k{i}_kernel<1>(int)",
+                                "Counter_Name": cname, "Counter_Value": part,
+                                "Start_Timestamp": t, "End_Timestamp": t + ns})
+            t += 2 * ns
+
+
+def test_mfma_summary(tmp_path):
+    # 100 us launches at 2.0 GHz: 200k cycles per XCD; stage i busy (i+1)/40 of them
+    per = []
+    busy_frac = []
+    for i, st in enumerate(T.STAGES):
+        f = (i + 1) / 40.0
+        for _ in range(T.STAGE_DISPATCHES.get(st, 1)):
+            per.append((f * T.N_SIMD * 200_000, 8 * 200_000))
+        busy_frac.append(f)
+    _write_mfma_run(tmp_path / "m", per)
+    s = T.summarize_mfma(str(tmp_path / "m"))
+    for i, st in enumerate(T.STAGES):
+        e = s["stages"][st]
+        assert e["clock_ghz"] == pytest.approx(2.0)
+        assert e["mfma_busy"] == pytest.approx(busy_frac[i])
+        assert e["mfma_busy_peak"] == pytest.approx(busy_frac[i] * 2.0 / 2.4)
+        assert e["se_busy"] == pytest.approx(1.0)
+    out = tmp_path / "m.md"
+    T.write_mfma_md(str(out), s, "cmd", "parse")
+    c = T.stage_counters(str(out), "dense.attn")
+    assert c["mfma_busy"] == pytest.approx(s["stages"]["dense.attn"]["mfma_busy"], rel=1e-5)
+    assert c["clock_ghz"] == pytest.approx(2.0)
