@@ -232,6 +232,24 @@ int sp_indexer_topk(const sp_problem *p, const void *q_idx, const void *k_idx, i
                     void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * sp_indexer_topk without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc). Same operation, arguments,
+ * output and requirements as sp_indexer_topk; the scratch lives in a static
+ * device array of the library, 64 MiB per GPU (SP_INDEXER_TOPK_STATIC_BYTES),
+ * held from the library's first use on that GPU until the process ends.
+ * Problems whose sp_workspace_bytes(p, SP_OP_INDEXER_TOPK) exceeds it
+ * (seq_len above about 20480) return SP_ERR_WORKSPACE before anything is
+ * enqueued. Nothing is allocated. Every call on one GPU shares that GPU's
+ * array: calls that may overlap on one GPU (on different streams, or from
+ * several host threads without ordering) race and must be serialised by the
+ * caller; calls ordered on one stream are safe.
+ */
+#define SP_INDEXER_TOPK_STATIC_BYTES (64u << 20)
+int sp_indexer_topk_noalloc(const sp_problem *p, const void *q_idx, const void *k_idx,
+                            int32_t *idx, hipStream_t stream);
+
+/*
  * Head-collapsed indexer front end (Section 6.3, the projection equations
  * and the score equation's RoPE; Algorithm 2, indexer projection and its key normalisation, RoPE and query scale): for token t at
  * position pos0 + t, with x_t = x[t,:],

@@ -109,6 +109,7 @@ def load() -> ctypes.CDLL:
         I32, F = ctypes.c_int32, ctypes.c_float
         lib.sp_indexer_project.argtypes = [PP, I32, I32, F, F, P, P, P, P, P, P, P, P]
         lib.sp_indexer_topk.argtypes = [PP, P, P, P, P, ctypes.c_size_t, P]
+        lib.sp_indexer_topk_noalloc.argtypes = [PP, P, P, P, P]
         lib.sp_sparse_gqa_attn_paged.argtypes = [PP, P, P, P, P, I32, I32, P, P, P]
         lib.sp_workspace_bytes.argtypes = [PP, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
         lib.sp_status_string.argtypes = [ctypes.c_int]
@@ -116,7 +117,7 @@ def load() -> ctypes.CDLL:
         lib.sp_version.argtypes = []
         for f in ("sp_dense_attn", "sp_oracle_support", "sp_indexer_scores", "sp_topk_select",
                   "sp_sparse_gqa_attn", "sp_kl_loss", "sp_indexer_project", "sp_indexer_topk",
-                  "sp_sparse_gqa_attn_paged",
+                  "sp_indexer_topk_noalloc", "sp_sparse_gqa_attn_paged",
                   "sp_workspace_bytes", "sp_version"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
@@ -226,6 +227,17 @@ def sp_indexer_topk(p: Problem, q_idx, k_idx, idx, workspace=None, stream=None) 
     _call("sp_indexer_topk", ctypes.byref(c), _ptr(q_idx, "q_idx", (S, di), bf),
           _ptr(k_idx, "k_idx", (S, di), bf), _ptr(idx, "idx", (S, p.topk), torch.int32),
           _ptr(workspace, "workspace", tuple(workspace.shape), workspace.dtype), nbytes,
+          _stream(stream))
+
+
+def sp_indexer_topk_noalloc(p: Problem, q_idx, k_idx, idx, stream=None) -> None:
+    """sp_indexer_topk with its scratch in the library's static device array
+    (no workspace; seq_len up to about 20480)."""
+    S, di = p.seq_len, p.index_dim
+    c = p.to_c()
+    bf = torch.bfloat16
+    _call("sp_indexer_topk_noalloc", ctypes.byref(c), _ptr(q_idx, "q_idx", (S, di), bf),
+          _ptr(k_idx, "k_idx", (S, di), bf), _ptr(idx, "idx", (S, p.topk), torch.int32),
           _stream(stream))
 
 

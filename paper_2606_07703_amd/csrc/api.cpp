@@ -223,6 +223,26 @@ int sp_indexer_topk(const sp_problem *p, const void *q_idx, const void *k_idx, i
   return launched(launch_indexer_topk(r, q_idx, k_idx, idx, workspace, stream));
 }
 
+int sp_indexer_topk_noalloc(const sp_problem *p, const void *q_idx, const void *k_idx,
+                            int32_t *idx, hipStream_t stream) {
+  SP_TRY(check_common(p));
+  SP_TRY(check_selection(p));
+  if (p->head_axis != 0) return SP_ERR_UNSUPPORTED;
+  if (p->index_dim != 64 && p->index_dim != 128 && p->index_dim != 256)
+    return SP_ERR_UNSUPPORTED;
+  if (p->relu != 0 && p->relu != 1) return SP_ERR_SHAPE;
+  if (p->block_q != 1) return SP_ERR_UNSUPPORTED;
+  if (p->q_offset != 0) return SP_ERR_UNSUPPORTED;
+  if (!q_idx || !k_idx || !idx) return SP_ERR_NULL;
+  if (!aligned16(q_idx) || !aligned16(k_idx) || !aligned16(idx)) return SP_ERR_ALIGN;
+  const Prob r = resolve(p);
+  if (!indexer_topk_supported(r)) return SP_ERR_UNSUPPORTED;
+  // the scratch this call needs must fit the library's static array
+  if (indexer_topk_workspace(r) > kIndexerTopkStaticBytes) return SP_ERR_WORKSPACE;
+  SP_TRY(check_device());
+  return launched(launch_indexer_topk_static(r, q_idx, k_idx, idx, stream));
+}
+
 int sp_indexer_project(const sp_problem *p, int32_t d_model, int32_t pos0, float rope_theta,
                        float ln_eps, const void *x, const void *w_q, const void *w_k,
                        const float *gamma, const float *beta, void *q_idx, void *k_idx,

@@ -26,6 +26,8 @@
 // MFMA chain and epilogue), which keeps the passes consistent.
 #include <math.h>
 
+#include <atomic>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "mfma.hpp"
@@ -519,9 +521,46 @@ hipError_t launch_di(const FzProb &f, const void *qi, const void *ki, int32_t *i
   return hipGetLastError();
 }
 
+// Scratch of the allocation-free entry point: one array per GPU the library
+// runs on, held until the process ends. Every call on a GPU shares it.
+static __device__ __align__(256) char scratch[kIndexerTopkStaticBytes];
+
+// Device address of this device's copy of `scratch`, looked up once per
+// device (with that device current) and kept. In host code the array's name
+// is only a stand-in for the symbol, never an address a kernel may use.
+constexpr int kScratchDevices = 64;
+std::atomic<void *> g_scratch[kScratchDevices];
+
+hipError_t static_scratch(void **out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+  void *ptr = g_scratch[dev].load(std::memory_order_acquire);
+  if (!ptr) {
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!ptr) return hipErrorInvalidSymbol;
+    g_scratch[dev].store(ptr, std::memory_order_release);
+  }
+  *out = ptr;
+  return hipSuccess;
+}
+
 }  // namespace
 
 size_t indexer_topk_workspace(const Prob &p) { return fz_bytes(p.S); }
+
+hipError_t launch_indexer_topk_static(const Prob &p, const void *qi, const void *ki,
+                                      int32_t *idx, hipStream_t st) {
+  if (fz_bytes(p.S) > kIndexerTopkStaticBytes) return hipErrorInvalidValue;   // checked by the API
+  void *ws = nullptr;
+  const hipError_t e = static_scratch(&ws);
+  if (e != hipSuccess) return e;
+  // every partial the passes read is written by an earlier pass of the same
+  // call (fz_init_kernel resets the per-row state), so no clearing is needed
+  return launch_indexer_topk(p, qi, ki, idx, ws, st);
+}
 
 bool indexer_topk_supported(const Prob &p) {
   return p.dtype == SP_DTYPE_BF16 && (p.di == 64 || p.di == 128 || p.di == 256) && p.b == 1 &&

@@ -83,6 +83,11 @@ bool indexer_topk_supported(const Prob &p);
 size_t indexer_topk_workspace(const Prob &p);
 hipError_t launch_indexer_topk(const Prob &p, const void *qi, const void *ki, int32_t *idx,
                                void *ws, hipStream_t st);
+// The same with its scratch in a static device array of this many bytes (per
+// GPU); problems whose workspace exceeds it are refused by the API.
+constexpr size_t kIndexerTopkStaticBytes = size_t(64) << 20;
+hipError_t launch_indexer_topk_static(const Prob &p, const void *qi, const void *ki,
+                                      int32_t *idx, hipStream_t st);
 hipError_t launch_kl_loss(int S, int n, const int32_t *rows, const float *P, const float *z,
                           float *kl, float *loss, float *grad, hipStream_t st);
 hipError_t launch_topk(const Prob &p, const float *scores, int32_t *idx, hipStream_t st);

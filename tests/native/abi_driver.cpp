@@ -168,6 +168,22 @@ int main() {
   CHECK(sp_indexer_topk(&p, addr(0), addr(1), (int32_t *)addr(2), addr(3), ws, nullptr) ==
         SP_OK);
   CHECK(sp_workspace_bytes(&p, 99, &ws) == SP_ERR_SHAPE);
+  // the allocation-free variant: same validation, its scratch bounded by the
+  // static array (the stand-in workspace is S * 1024 bytes)
+  CHECK(sp_indexer_topk_noalloc(&p, addr(0), addr(1), (int32_t *)addr(2), nullptr) == SP_OK &&
+        strcmp(stub::last, "indexer_topk_static") == 0);
+  p.seq_len = 65535;   // 64 MiB of stand-in workspace: exactly at the bound
+  CHECK(sp_indexer_topk_noalloc(&p, addr(0), addr(1), (int32_t *)addr(2), nullptr) == SP_OK);
+  p.seq_len = 65536;   // past the fused kernel's limit
+  CHECK(sp_indexer_topk_noalloc(&p, addr(0), addr(1), (int32_t *)addr(2), nullptr) ==
+        SP_ERR_UNSUPPORTED);
+  p = base();
+  p.block_q = 1;
+  CHECK(sp_indexer_topk_noalloc(&p, nullptr, addr(1), (int32_t *)addr(2), nullptr) ==
+        SP_ERR_NULL);
+  p.block_q = 4;
+  CHECK(sp_indexer_topk_noalloc(&p, addr(0), addr(1), (int32_t *)addr(2), nullptr) ==
+        SP_ERR_UNSUPPORTED);
 
   // KL and the front end
   p = base();

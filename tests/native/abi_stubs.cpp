@@ -32,6 +32,12 @@ hipError_t hipGetLastError(void) { return hipSuccess; }
 
 namespace sp {
 namespace {
+hipError_t record(const char *name, const Prob &p);
+}  // namespace
+}  // namespace sp
+
+namespace sp {
+namespace {
 hipError_t record(const char *name, const Prob &p) {
   stub::last = name;
   stub::prob = p;
@@ -101,5 +107,12 @@ hipError_t launch_kl_loss(int S, int, const int32_t *, const float *, const floa
 }
 hipError_t launch_topk(const Prob &p, const float *, int32_t *, hipStream_t) {
   return record("topk", p);
+}
+}  // namespace sp
+
+namespace sp {
+hipError_t launch_indexer_topk_static(const Prob &p, const void *, const void *, int32_t *,
+                                      hipStream_t) {
+  return record("indexer_topk_static", p);
 }
 }  // namespace sp

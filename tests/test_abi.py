@@ -238,3 +238,14 @@ def test_oracle_support_and_fused_reject_chunks():
     p = prob(q_offset=8, block_q=1)
     n = ctypes.c_size_t()
     assert lib().sp_indexer_topk(ctypes.byref(p), A, A2, A3, A4, 1 << 30, None) == UNSUP
+
+
+def test_noalloc_refuses_problems_beyond_its_static_scratch():
+    # about 20480 tokens fit the 64 MiB array; refused before any device call
+    p = prob(seq_len=30000, block_q=1, index_dim=128, topk=64)
+    assert rc("sp_indexer_topk_noalloc", p, A, A2, A3, None) == WS
+    p = prob(seq_len=30000, block_q=4, index_dim=128, topk=64)
+    assert rc("sp_indexer_topk_noalloc", p, A, A2, A3, None) == UNSUP
+    assert rc("sp_indexer_topk_noalloc", prob(block_q=1), None, A2, A3, None) == NULL
+    if NO_DEVICE:
+        assert rc("sp_indexer_topk_noalloc", prob(block_q=1), A, A2, A3, None) == NODEV
