@@ -56,8 +56,6 @@ MFMA_SUMMARY = os.path.join(PROFILES, "mfma_headline_32k.md")
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 FP32_VALU_PEAK_TFLOPS = 157.3
-# fp64 rate of the oracle on a many-core host, used only to size CPU samples
-CPU_PLAN_FLOPS = 3e10
 METRIC = "ms/layer sparse GQA prefill @32K, speedup vs own dense, % HBM/MFMA roofline"
 ALL_WORKLOADS = ("oracle_tiny_512", "indexer_4k", "block_16k", "headline_32k", "stress_100k")
 
@@ -76,6 +74,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=8.0,
                     help="rough CPU time per oracle leg (bounded samples)")
+    ap.add_argument("--summary-out", default=None,
+                    help="also write a Markdown table of the workloads' lines to this file")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one device copy of this size (the calibration "
                          "kernel for rocprofv3 FETCH_SIZE/WRITE_SIZE runs)")
@@ -432,9 +432,19 @@ def run_workload(args, name):
     print(json.dumps(out), flush=True)
     del plan, dev, inp
     torch.cuda.empty_cache()
+    return out
 
 
 def cpu_model() -> str:
+    """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for ln in out.splitlines():
+            if ln.strip().startswith("Model name:"):
+                return ln.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
     try:
         for ln in open("/proc/cpuinfo"):
             if ln.startswith("model name"):
@@ -473,16 +483,7 @@ def cpu_baseline(plan, inp, counts, seconds):
         r = fn()
         return r, time.perf_counter() - t0
 
-    def selection_leg(mode, prefix, b, agg="max", W=0, qi=None, ki=None):
-        R = (S + b - 1) // b
-        L = np.minimum(np.arange(R) * b + b, S).astype(np.float64)
-        # sample size: aim for about `seconds` of CPU time (flops per block
-        # of scoring and restricted attention at a planning rate)
-        hd = w.head_dim * w.num_q_heads
-        score = 2 * w.index_dim if mode == "indexer" else 4 * hd
-        per_unit = b * (L.mean() * score + 4 * min(k, L.mean()) * hd) / CPU_PLAN_FLOPS
-        n = int(max(4, min(R, seconds / max(per_unit, 1e-9))))
-        units = _spread(R, n)
+    def run_units(mode, units, b, agg, W, qi, ki, R):
         if mode == "indexer":
             Y, t_sc = timed(lambda: oracle.support_scores("indexer", units, b, q_idx=qi, k_idx=ki,
                                                           agg=agg))
@@ -493,6 +494,19 @@ def cpu_baseline(plan, inp, counts, seconds):
         table[units] = sel
         rows = np.concatenate([np.arange(u * b, min(u * b + b, S)) for u in units])
         _, t_sp = timed(lambda: oracle.sparse(q64, k64, v64, table, b, rows=rows))
+        return table, t_sc, t_tk, t_sp
+
+    def selection_leg(mode, prefix, b, agg="max", W=0, qi=None, ki=None):
+        R = (S + b - 1) // b
+        L = np.minimum(np.arange(R) * b + b, S).astype(np.float64)
+        # sample size: time two blocks from the middle of the sequence, then
+        # take as many evenly spaced blocks as fill about `seconds`
+        probe = np.array([R // 2, min(R - 1, R // 2 + 1)])
+        _, a, c, e = run_units(mode, probe, b, agg, W, qi, ki, R)
+        per_unit = (a + c + e) / len(probe) * L.mean() / L[probe].mean()
+        n = int(max(4, min(R, seconds / max(per_unit, 1e-9))))
+        units = _spread(R, n)
+        table, t_sc, t_tk, t_sp = run_units(mode, units, b, agg, W, qi, ki, R)
         # kept pairs of the sampled blocks under the oracle's own selection
         pairs_s = 0
         for u in units:
@@ -508,7 +522,9 @@ def cpu_baseline(plan, inp, counts, seconds):
         return ms
 
     def dense_leg():
-        per_row = 4.0 * S / 2 * w.head_dim * w.num_q_heads / CPU_PLAN_FLOPS
+        probe = np.array([S // 2, S // 2 + 1]) if S > 2 else np.arange(S)
+        _, t = timed(lambda: oracle.dense(q64, k64, v64, rows=probe))
+        per_row = t / len(probe) * (S / 2) / max(float(probe.mean()) + 1, 1.0)
         n = int(max(4, min(S, seconds / max(per_row, 1e-9))))
         rows = _spread(S, n, include=[S - 1])
         _, t = timed(lambda: oracle.dense(q64, k64, v64, rows=rows))
@@ -547,8 +563,41 @@ def main():
               "(the path shards by selection blocks, see the design notes)", file=sys.stderr)
         sys.exit(2)
     names = ALL_WORKLOADS if args.workload == "all" else (args.workload,)
-    for n in names:
-        run_workload(args, n)
+    lines = [run_workload(args, n) for n in names]
+    if args.summary_out:
+        write_summary(args, lines)
+
+
+def write_summary(args, lines):
+    """Markdown table of the workloads' bench lines (modes, rooflines, CPU legs)."""
+    cmd = "python3 -u bench.py --workload " + args.workload + \
+        f" --steps {args.steps} --warmup {args.warmup}" + \
+        (" --no-cpu-baseline" if args.no_cpu_baseline else "")
+    L = ["# Bench lines of every workload", "", "Command (repository root, one MI355X):", "",
+         "    " + cmd, "",
+         "ms/layer are medians of the timed steps (HIP events on the launch stream); the "
+         "roofline fraction is the dominant kernel of the measured mode; CPU legs are the fp64 "
+         "oracle on bounded samples of the same workload, scaled to a layer.", "",
+         "| workload | measured mode | ms/layer | dense ms | speedup | other modes (ms/layer) "
+         "| dominant kernel: roofline | CPU oracle ms/layer (cores) |",
+         "|---|---|---:|---:|---:|---|---|---|"]
+    for d in lines:
+        cfg = d["config"]
+        others = ", ".join(f"{m} {v}" for m, v in d["modes_ms_per_layer"].items()
+                           if m not in (cfg["selection"], "dense"))
+        r = d["roofline"]
+        cpu = d["cpu_baseline"]
+        cpu_s = "—" if not cpu else (f"{cpu['value']} ({cpu['cores']}); " + ", ".join(
+            f"{k} {v['ms_per_layer']}" for k, v in cpu["legs"].items()))
+        L.append(f"| {cfg['workload']} (S={cfg['seq_len']}, b={cfg['block_q']}, k={cfg['topk']}) "
+                 f"| {cfg['selection']} | {d['value']} | {d['dense_ms']} | {d['speedup_vs_dense']} "
+                 f"| {others or '—'} | {r['kernel']}: {r['frac']} of {r['peak']} {r['unit']} "
+                 f"| {cpu_s} |")
+    L.append("")
+    L.append("Per-kernel figures (ms median, roofline fractions) are in each line's `kernels` "
+             "object; the CPU host was " + (lines[0]["cpu_baseline"] or {}).get("cpu_model", "—")
+             + ".")
+    open(args.summary_out, "w").write("\n".join(L) + "\n")
 
 
 if __name__ == "__main__":

@@ -49,7 +49,7 @@ struct SupportKeys {
 
 template <int D, int NW, bool PAGED>
 __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel(
-    int S, int Hq, int Hkv, int G, int b, int kk, int R, size_t gstride, float scale_log2,
+    int S, int Hq, int Hkv, int G, int b, int kk, int nchunks, size_t gstride, float scale_log2,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const int32_t *__restrict__ idx,
     uint16_t *__restrict__ o, KvPages pages, int qo) {
@@ -65,10 +65,12 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int h = lane >> 5, n = lane & 31;
+  // the row chunks of one (block, KV head) are Hkv workgroups apart: the same
+  // XCD, dispatched together, so the second gathers its rows from that L2
   const int j = (int)blockIdx.x % Hkv;
   const int rest = (int)blockIdx.x / Hkv;
-  const int r = rest % R;   // counts blocks from the chunk start
-  const int chunk = rest / R;
+  const int chunk = rest % nchunks;
+  const int r = rest / nchunks;   // counts blocks from the chunk start
   const int t0 = qo + r * b;
   const int t1 = min(t0 + b, S) - 1;
   const int nrows = (t1 - t0 + 1) * G;
@@ -173,7 +175,7 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
   uint16_t *os = (uint16_t *)o - shift;
 #define SP_SB(NW)                                                                            \
   hipLaunchKernelGGL((sparse_block_kernel<D, NW, PAGED>), grid, dim3(NW * 64), 0, st, p.S,  \
-                     p.Hq, p.Hkv, p.G, p.b, p.k, p.R, p.idx_group_stride(), sl2,              \
+                     p.Hq, p.Hkv, p.G, p.b, p.k, chunks, p.idx_group_stride(), sl2,           \
                      qs, (const uint16_t *)k, (const uint16_t *)v, idx, os, pages, p.qo)
   switch (nw) {
     case 1: SP_SB(1); break;

@@ -30,23 +30,63 @@ constexpr uint32_t kZeroKey = 0x80000000u;   // float_key(+0.0f)
 __device__ __forceinline__ int digit_shift(int pass) { return pass == 0 ? 21 : (pass == 1 ? 10 : 0); }
 __device__ __forceinline__ int digit_bits(int pass) { return pass == 2 ? 10 : 11; }
 
-// Given a filled histogram of nb bins, find the bin holding the
-// `remaining`-th largest key; writes (bin, rank within bin) to sel.
-// Every thread must call it (it contains barriers).
-template <int NT>
+// Exclusive prefix over a block of NT threads of per-thread values whose set
+// bits all lie in MASK, and the block total: bit-sliced wave ballots (no LDS
+// round trips inside a wave), then one barrier to combine the wave totals.
+// `row` selects a scratch row: consecutive scans must alternate rows (a row
+// is written again only after the barrier of the scan in between).
+template <int NT, uint32_t MASK>
+__device__ __forceinline__ uint32_t scan_bits(uint32_t v, uint32_t (*scratch)[NT / 64], int row,
+                                              uint32_t *total) {
+  constexpr int NW = NT / 64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t excl = 0, wtot = 0;
+#pragma unroll
+  for (int bit = 0; bit < 32; ++bit) {
+    if (!((MASK >> bit) & 1u)) continue;
+    const uint64_t m = __ballot((v >> bit) & 1u);
+    excl += __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                      __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u)) << bit;
+    wtot += (uint32_t)__popcll(m) << bit;
+  }
+  if (lane == 0) scratch[row][wave] = wtot;
+  __syncthreads();
+  uint32_t base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const uint32_t t = scratch[row][w];
+    base += w < wave ? t : 0u;
+    tot += t;
+  }
+  *total = tot;
+  return base + excl;
+}
+
+// Given NC interleaved copies of a filled histogram of nb bins (bin i of
+// copy c at hist[i*NC + c]), find the bin holding the `remaining`-th largest
+// key; writes (bin, rank within bin) to sel. Every thread must call it (it
+// contains barriers).
+template <int NT, int NC = 1>
 __device__ __forceinline__ void find_digit(const uint32_t *hist, int nb, uint32_t remaining,
-                                           uint32_t *scan_scratch, uint32_t *sel) {
+                                           uint32_t (*scratch)[NT / 64], int row,
+                                           uint32_t *sel) {
   const int tid = threadIdx.x;
   const int per = nb / NT;            // nb is a multiple of NT
   const int hi = nb - tid * per;      // thread 0 owns the highest bins
+  auto bin = [&](int i) {
+    uint32_t c = 0;
+#pragma unroll
+    for (int x = 0; x < NC; ++x) c += hist[i * NC + x];
+    return c;
+  };
   uint32_t mine = 0;
-  for (int i = hi - per; i < hi; ++i) mine += hist[i];
+  for (int i = hi - per; i < hi; ++i) mine += bin(i);
   uint32_t total;
-  const uint32_t above = block_exclusive_scan<NT>(mine, scan_scratch, &total);
+  const uint32_t above = scan_bits<NT, 0xffffu>(mine, scratch, row, &total);
   if (above < remaining && above + mine >= remaining) {
     uint32_t acc = above;
     for (int i = hi - 1; i >= hi - per; --i) {
-      const uint32_t c = hist[i];
+      const uint32_t c = bin(i);
       if (acc + c >= remaining) {
         sel[0] = (uint32_t)i;
         sel[1] = remaining - acc;
@@ -63,13 +103,19 @@ constexpr int kRegNT = 512;
 constexpr int kRun = 16;                      // consecutive positions per run
 constexpr int kRegSub = 4;                    // runs per thread
 constexpr int kRegCap = kRegNT * kRun * kRegSub;   // 32768 candidates
+// The first digit's histogram has kCopies interleaved copies, lane l counting
+// into copy l % kCopies: block-aggregated scores crowd into a few top bins,
+// and the copies (adjacent words, so different banks) cut the conflicts of
+// one wave's atomics on them; the later digits, over keys sharing the first,
+// spread out and use one copy.
+constexpr int kCopies = 4;
 
 __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int qo, int b, int k, int W,
                                                           const float *__restrict__ scores,
                                                           int32_t *__restrict__ idx) {
   constexpr int NT = kRegNT;
-  __shared__ uint32_t hist[2048];
-  __shared__ uint32_t scan_scratch[NT / 64 + 1];
+  __shared__ uint32_t hist[kCopies * 2048];
+  __shared__ uint32_t scratch[2][NT / 64];
   __shared__ uint32_t sel[2];
 
   const int r = blockIdx.x;
@@ -121,7 +167,9 @@ __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int qo, int b, 
     for (int pass = 0; pass < 3; ++pass) {
       const int shift = digit_shift(pass), nb = 1 << digit_bits(pass);
       const uint32_t dmask = (uint32_t)nb - 1u;
-      for (int i = tid; i < nb; i += NT) hist[i] = 0;
+      const int nco = pass == 0 ? kCopies : 1;   // histogram copies of this digit
+      uint32_t *hc = hist + (pass == 0 ? lane % kCopies : 0);
+      for (int i = tid; i < nb * nco; i += NT) hist[i] = 0;
       __syncthreads();
       uint32_t zc = 0;
 #pragma unroll
@@ -133,17 +181,20 @@ __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int qo, int b, 
           const uint32_t kv = key[j][i];
           if (p0 + i < nc && (kv & pmask) == prefix) {
             if (kv == kZeroKey) ++zc;
-            else atomicAdd(&hist[(kv >> shift) & dmask], 1u);
+            else atomicAdd(&hc[((kv >> shift) & dmask) * nco], 1u);
           }
         }
       }
       if ((kZeroKey & pmask) == prefix) {
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) zc += __shfl_xor(zc, off, 64);
-        if (lane == 0 && zc) atomicAdd(&hist[(kZeroKey >> shift) & dmask], zc);
+        if (lane == 0 && zc) atomicAdd(&hist[((kZeroKey >> shift) & dmask) * nco], zc);
       }
       __syncthreads();
-      find_digit<NT>(hist, nb, remaining, scan_scratch, sel);
+      if (pass == 0)
+        find_digit<NT, kCopies>(hist, nb, remaining, scratch, 0, sel);
+      else
+        find_digit<NT>(hist, nb, remaining, scratch, pass & 1, sel);
       prefix |= sel[0] << shift;
       pmask |= dmask << shift;
       remaining = sel[1];
@@ -168,7 +219,8 @@ __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int qo, int b, 
       }
     }
     uint32_t total;
-    const uint32_t ex = block_exclusive_scan<NT>((cgt << 16) | ceq, scan_scratch, &total);
+    // counts of at most 16 each: bits 0..4 and 16..20
+    const uint32_t ex = scan_bits<NT, 0x1f001fu>((cgt << 16) | ceq, scratch, (j + 1) & 1, &total);
     const uint32_t my_gt = gt_before + (ex >> 16);
     uint32_t my_eq = eq_before + (ex & 0xffffu);
     uint32_t pos = my_gt + min(my_eq, remaining);
@@ -203,7 +255,7 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, in
                                                         const float *__restrict__ scores,
                                                         int32_t *__restrict__ idx) {
   __shared__ uint32_t hist[2048];
-  __shared__ uint32_t scan_scratch[kNT / 64 + 1];
+  __shared__ uint32_t scratch[2][kNT / 64];
   __shared__ uint32_t sel[2];
   __shared__ uint32_t keys[kEmitPer * kEmitStride];
 
@@ -249,7 +301,7 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, in
         if (lane == 0 && zc) atomicAdd(&hist[(kZeroKey >> shift) & dmask], zc);
       }
       __syncthreads();
-      find_digit<kNT>(hist, nb, remaining, scan_scratch, sel);
+      find_digit<kNT>(hist, nb, remaining, scratch, pass & 1, sel);
       prefix |= sel[0] << shift;
       pmask |= dmask << shift;
       remaining = sel[1];
@@ -261,7 +313,8 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, in
   // Ordered emission over candidates in chunks of kEmitChunk positions; in
   // LDS, position q of a chunk sits at (q % kEmitPer) * kEmitStride + q / kEmitPer.
   uint32_t gt_before = 0, eq_before = 0;
-  for (int base = 0; base < nc; base += kEmitChunk) {
+  int srow = 1;
+  for (int base = 0; base < nc; base += kEmitChunk, srow ^= 1) {
     const int n = min(kEmitChunk, nc - base);
     for (int i = tid; i < kEmitChunk; i += kNT)
       keys[(i % kEmitPer) * kEmitStride + i / kEmitPer] = i < n ? float_key(row[base + i]) : 0u;
@@ -277,7 +330,7 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, in
       }
     }
     uint32_t total;
-    const uint32_t ex = block_exclusive_scan<kNT>((cgt << 16) | ceq, scan_scratch, &total);
+    const uint32_t ex = scan_bits<kNT, 0x1f001fu>((cgt << 16) | ceq, scratch, srow, &total);
     uint32_t my_gt = gt_before + (ex >> 16);
     uint32_t my_eq = eq_before + (ex & 0xffffu);
     uint32_t pos = my_gt + min(my_eq, remaining);

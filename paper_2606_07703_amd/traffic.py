@@ -296,6 +296,34 @@ def stage_counters(path: str, stage: str) -> Optional[Dict]:
     return None
 
 
+# ------------------------------------------------------------ kernel times
+def write_stats_md(path: str, stats_csv: str, bench_json: str, cmd: str) -> None:
+    """Kernel-time summary of a rocprofv3 --kernel-trace --stats run of the
+    bench, with the bench line of the same run for the roofline cross-check."""
+    import json
+    rows = list(csv.DictReader(open(stats_csv)))
+    line = json.loads([ln for ln in open(bench_json) if ln.startswith("{")][-1])
+    roof = line["roofline"]
+    total = sum(float(r["TotalDurationNs"]) for r in rows)
+    L = ["# Kernel-time summary: headline 32K workload, every bench stage", "",
+         "Workload: S=32768, Hq=32, Hkv=8, d=128, d_idx=128, top-k 2048, bf16 (bench.py's "
+         "headline_32k step: front end, indexer mode with 64-query blocks (contiguous and "
+         "paged K/V), per query (unfused and fused), dense, oracle mode and the KL "
+         "objective).", "",
+         "Command (repository root, one MI355X):", "", "    " + cmd, "",
+         f"Roofline cross-check: the bench line of this run measured `{roof['kernel']}` with HIP "
+         f"events at {roof['launch_ms']} ms per launch; its kernel's average below comes from "
+         "the trace of the same launches (warmup included).", "",
+         "| kernel | calls | avg ms | min ms | max ms | share of GPU time |",
+         "|---|---:|---:|---:|---:|---:|"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        name = _short(r["Name"]) if "sp::" in r["Name"] else r["Name"].split("(")[0][:60]
+        L.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e6:.4f} | "
+                 f"{float(r['MinNs']) / 1e6:.4f} | {float(r['MaxNs']) / 1e6:.4f} | "
+                 f"{100 * float(r['TotalDurationNs']) / total:.2f}% |")
+    open(path, "w").write("\n".join(L) + "\n")
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--fetch", help="rocprofv3 output dir of the FETCH_SIZE run")
@@ -307,7 +335,14 @@ def main(argv=None):
     ap.add_argument("--mfma", help="rocprofv3 output dir of the matrix-core counter run "
                                    "(writes the utilisation summary instead)")
     ap.add_argument("--cmd-mfma")
+    ap.add_argument("--stats", help="kernel_stats.csv of a --kernel-trace --stats run "
+                                    "(writes the kernel-time summary instead)")
+    ap.add_argument("--bench-json", help="the bench line of that run")
+    ap.add_argument("--cmd-stats")
     a = ap.parse_args(argv)
+    if a.stats:
+        write_stats_md(a.out, a.stats, a.bench_json, a.cmd_stats or "")
+        return
     if a.mfma:
         s = summarize_mfma(a.mfma)
         parse_cmd = (f"python3 -m paper_2606_07703_amd.traffic --mfma {a.mfma} --out {a.out} "

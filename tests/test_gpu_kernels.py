@@ -202,6 +202,10 @@ TOPK_CASES = [
     (5000, 64, 512, 0, "relu"),
     (9000, 128, 2048, 128, "gauss"),
     (9000, 128, 700, 0, "coarse"),
+    (20000, 64, 2048, 0, "const"),     # every key on the threshold: no compaction
+    (30000, 64, 9000, 0, "gauss"),     # more chosen than the LDS staging holds
+    (32768, 64, 2048, 0, "relu"),      # the 32K block shape, ReLU zeros
+    (30000, 64, 512, 16, "coarse"),    # long rows of 16 levels: crowded bins
 ]
 
 
