@@ -194,7 +194,7 @@ int sp_sparse_gqa_attn(const sp_problem *p, const void *q, const void *k, const 
     return SP_ERR_ALIGN;
   SP_TRY(check_device());
   const Prob r = resolve(p);
-  if (sparse_block_mfma_supported(r))
+  if (sparse_block_mfma_supported(r, false))
     return launched(launch_sparse_block_mfma(r, q, k, v, idx, o, stream));
   if (sparse_query_mfma_supported(r))
     return launched(launch_sparse_query_mfma(r, q, k, v, idx, o, stream));
@@ -300,7 +300,7 @@ int sp_sparse_gqa_attn_paged(const sp_problem *p, const void *q, const void *k_p
   pages.table = page_table;
   pages.page_size = page_size;
   pages.num_pages = num_pages;
-  if (sparse_block_mfma_supported(r))
+  if (sparse_block_mfma_supported(r, true))
     return launched(launch_sparse_block_mfma(r, q, k_pages, v_pages, idx, o, stream, pages));
   if (sparse_query_mfma_supported(r))
     return launched(launch_sparse_query_mfma(r, q, k_pages, v_pages, idx, o, stream, pages));

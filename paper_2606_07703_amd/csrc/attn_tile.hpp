@@ -46,8 +46,16 @@ namespace sp {
 // The attention workgroups fill most of a CU's LDS, so at most two waves
 // share a SIMD; telling the compiler so lets it spend up to 256 registers a
 // wave on operand prefetch instead of trimming for an occupancy it cannot
-// reach.
-#define SP_ATTN_OCCUPANCY __attribute__((amdgpu_waves_per_eu(1, 2)))
+// reach. At head_dim 256 a wave's accumulators and query operands alone take
+// 192 registers: those workgroups run one wave per SIMD (up to 512).
+#define SP_ATTN_OCCUPANCY(D) __attribute__((amdgpu_waves_per_eu(1, (D) == 256 ? 1 : 2)))
+
+// Waves per attention workgroup at head dimension D: two groups of four
+// (one wave of each per SIMD) up to 128, one group at 256.
+template <int D>
+constexpr int attn_max_waves() {
+  return D == 256 ? 4 : 8;
+}
 
 // Operand pairs of the matrix phase read ahead of the products.
 constexpr int kMPrefetch = 2;

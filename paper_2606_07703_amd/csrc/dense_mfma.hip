@@ -2,9 +2,10 @@
 // Algorithm 1, dense scores and normalisers): a flash-attention forward that also returns the
 // softmax normaliser lse[t,h] = log sum_{s<=t} exp(scale <q[t,h], k[s,g(h)]>).
 //
-// One workgroup per (tile of 256/G queries, KV head j): its 256 query rows are
-// every (query, head) pair of the tile with g(h) = j, so each K/V tile staged
-// in LDS serves all G heads of the group. Key tiles below a wave's first
+// One workgroup per (tile of 256/G queries, KV head j; 128/G at head_dim
+// 256): its 256 (128) query rows are every (query, head) pair of the tile
+// with g(h) = j, so each K/V tile staged in LDS serves all G heads of the
+// group. Key tiles below a wave's first
 // query need no mask; only tiles reaching the diagonal apply s <= t.
 // Workgroups are numbered with the KV head fastest, so consecutive
 // workgroups (which the dispatcher spreads over the XCDs) keep one head per
@@ -18,8 +19,6 @@
 
 namespace sp {
 namespace {
-
-constexpr int kNW = 8;
 
 struct DenseKeys {
   static constexpr bool kLookup = false;   // rows are arithmetic
@@ -35,11 +34,12 @@ struct DenseKeys {
 };
 
 template <int D, bool WANT_O>
-__global__ __launch_bounds__(kNW * 64) SP_ATTN_OCCUPANCY void dense_fwd_kernel(
+__global__ __launch_bounds__(attn_max_waves<D>() * 64) SP_ATTN_OCCUPANCY(D) void dense_fwd_kernel(
     int S, int Hq, int Hkv, int G, int TQ, int nqt, float scale_log2,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, uint16_t *__restrict__ o, float *__restrict__ lse) {
   using L = AttnLayout<D>;
+  constexpr int kNW = attn_max_waves<D>();
   __shared__ __align__(16) char lds[L::bytes(WANT_O)];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -65,6 +65,7 @@ __global__ __launch_bounds__(kNW * 64) SP_ATTN_OCCUPANCY void dense_fwd_kernel(
 template <int D>
 hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v, void *o,
                     float *lse, hipStream_t st) {
+  constexpr int kNW = attn_max_waves<D>();
   const int TQ = (kNW * kAttnQPW) / p.G;
   const int nqt = (p.S + TQ - 1) / TQ;
   dim3 grid(nqt * p.Hkv);
@@ -83,12 +84,14 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v, 
 }  // namespace
 
 bool dense_mfma_supported(const Prob &p) {
-  return p.dtype == SP_DTYPE_BF16 && (p.d == 64 || p.d == 128) && p.G <= kNW * kAttnQPW;
+  return p.dtype == SP_DTYPE_BF16 && (p.d == 64 || p.d == 128 || p.d == 256) &&
+         p.G <= (p.d == 256 ? attn_max_waves<256>() : attn_max_waves<128>()) * kAttnQPW;
 }
 
 hipError_t launch_dense_mfma(const Prob &p, const void *q, const void *k, const void *v,
                              void *o, float *lse, hipStream_t st) {
   if (p.d == 64) return launch_d<64>(p, q, k, v, o, lse, st);
+  if (p.d == 256) return launch_d<256>(p, q, k, v, o, lse, st);
   return launch_d<128>(p, q, k, v, o, lse, st);
 }
 

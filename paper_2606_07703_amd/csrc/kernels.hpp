@@ -47,7 +47,8 @@ bool sparse_query_mfma_supported(const Prob &p);
 hipError_t launch_sparse_query_mfma(const Prob &p, const void *q, const void *k, const void *v,
                                     const int32_t *idx, void *o, hipStream_t st,
                                     KvPages pages = KvPages());
-bool sparse_block_mfma_supported(const Prob &p);
+// paged: K/V read through a page table (a smaller support fits LDS at d = 256)
+bool sparse_block_mfma_supported(const Prob &p, bool paged);
 hipError_t launch_sparse_block_mfma(const Prob &p, const void *q, const void *k, const void *v,
                                     const int32_t *idx, void *o, hipStream_t st,
                                     KvPages pages = KvPages());

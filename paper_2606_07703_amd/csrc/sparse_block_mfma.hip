@@ -3,7 +3,7 @@
 // and Algorithm 2, selection and sparse GQA prefill: one support per block, replicated over KV heads).
 //
 // One workgroup per (selection block r, KV head j, chunk of up to 256 query
-// rows). A query row is a (query t, head h) pair with g(h) = j; there are
+// rows; 128 at head_dim 256). A query row is a (query t, head h) pair with g(h) = j; there are
 // b*G of them per (r, j), ordered query-major. The support idx[r] is walked
 // in tiles of 64 entries: the workgroup gathers the 64 selected K rows and
 // V rows of head j into LDS once, and every wave reuses them for its 32 query
@@ -23,8 +23,11 @@
 namespace sp {
 namespace {
 
-constexpr int kMaxSupport = 4096;   // support row cached in LDS (a multiple of the tile)
-constexpr int kMaxTiles = kMaxSupport / kAttnKT;
+// Support entries cached in LDS (a multiple of the tile): 4096, except for
+// the paged cache at head_dim 256, whose K/V tiles and second row table leave
+// room for 2048.
+constexpr int max_support(int D, bool paged) { return D == 256 && paged ? 2048 : 4096; }
+constexpr int kMaxTiles = 4096 / kAttnKT;
 
 // The usable support entries in LDS: positions (pos), K/V rows (row: the
 // position, or its paged-cache row), and which tiles need the causal mask
@@ -48,7 +51,7 @@ struct SupportKeys {
 };
 
 template <int D, int NW, bool PAGED>
-__global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel(
+__global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY(D) void sparse_block_kernel(
     int S, int Hq, int Hkv, int G, int b, int kk, int nchunks, size_t gstride, float scale_log2,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const int32_t *__restrict__ idx,
@@ -56,6 +59,7 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY void sparse_block_kernel
   // q and o are addressed by position: the host shifts them back by qo rows
   using L = AttnLayout<D>;
   constexpr int NT = NW * 64;
+  constexpr int kMaxSupport = max_support(D, PAGED);
   __shared__ __align__(16) char lds[L::bytes(true)];
   __shared__ int red_cnt[2][NW];
   __shared__ __align__(16) int ir[kMaxSupport];
@@ -166,7 +170,10 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
                     const int32_t *idx, void *o, hipStream_t st, KvPages pages) {
   const int rows = p.b * p.G;
   int nw = (rows + kAttnQPW - 1) / kAttnQPW;
-  nw = nw <= 1 ? 1 : nw <= 2 ? 2 : nw <= 4 ? 4 : 8;
+  nw = nw <= 1 ? 1 : nw <= 2 ? 2 : nw <= 4 ? 4 : attn_max_waves<D>();
+  // at head_dim 256 a wave's share of the tile loads grows with fewer waves
+  // (69 chunks for one) and its row registers no longer fit: always four
+  if (D == 256) nw = 4;
   const int chunks = (rows + nw * kAttnQPW - 1) / (nw * kAttnQPW);
   dim3 grid(p.R * p.Hkv * chunks);
   const float sl2 = p.scale * kLog2e;
@@ -177,11 +184,15 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
   hipLaunchKernelGGL((sparse_block_kernel<D, NW, PAGED>), grid, dim3(NW * 64), 0, st, p.S,  \
                      p.Hq, p.Hkv, p.G, p.b, p.k, chunks, p.idx_group_stride(), sl2,           \
                      qs, (const uint16_t *)k, (const uint16_t *)v, idx, os, pages, p.qo)
-  switch (nw) {
-    case 1: SP_SB(1); break;
-    case 2: SP_SB(2); break;
-    case 4: SP_SB(4); break;
-    default: SP_SB(8); break;
+  if constexpr (D == 256) {
+    SP_SB(4);
+  } else {
+    switch (nw) {
+      case 1: SP_SB(1); break;
+      case 2: SP_SB(2); break;
+      case 4: SP_SB(4); break;
+      default: SP_SB(8); break;
+    }
   }
 #undef SP_SB
   return hipGetLastError();
@@ -189,18 +200,20 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
 
 }  // namespace
 
-bool sparse_block_mfma_supported(const Prob &p) {
-  return p.dtype == SP_DTYPE_BF16 && (p.d == 64 || p.d == 128) && p.b >= 16 &&
-         p.k <= kMaxSupport;
+bool sparse_block_mfma_supported(const Prob &p, bool paged) {
+  return p.dtype == SP_DTYPE_BF16 && (p.d == 64 || p.d == 128 || p.d == 256) && p.b >= 16 &&
+         p.k <= max_support(p.d, paged);
 }
 
 hipError_t launch_sparse_block_mfma(const Prob &p, const void *q, const void *k, const void *v,
                                     const int32_t *idx, void *o, hipStream_t st, KvPages pages) {
   if (pages.table) {
     if (p.d == 64) return launch_d<64, true>(p, q, k, v, idx, o, st, pages);
+    if (p.d == 256) return launch_d<256, true>(p, q, k, v, idx, o, st, pages);
     return launch_d<128, true>(p, q, k, v, idx, o, st, pages);
   }
   if (p.d == 64) return launch_d<64, false>(p, q, k, v, idx, o, st, pages);
+  if (p.d == 256) return launch_d<256, false>(p, q, k, v, idx, o, st, pages);
   return launch_d<128, false>(p, q, k, v, idx, o, st, pages);
 }
 

@@ -55,7 +55,7 @@ hipError_t launch_sparse_query_mfma(const Prob &p, const void *, const void *, c
                                     const int32_t *, void *, hipStream_t, KvPages) {
   return record("sparse_query_mfma", p);
 }
-bool sparse_block_mfma_supported(const Prob &p) {
+bool sparse_block_mfma_supported(const Prob &p, bool) {
   return p.dtype == SP_DTYPE_BF16 && p.b >= 16;
 }
 hipError_t launch_sparse_block_mfma(const Prob &p, const void *, const void *, const void *,

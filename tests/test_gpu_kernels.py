@@ -84,7 +84,11 @@ SHARP_CASES = [
     (1500, 8, 2, 64, "bf16", 4, 700, True),         # per-query kernel, b = 4, shuffled
     (1200, 4, 2, 64, "f32", 1, 500, False),         # row-wise, fp32
     (700, 34, 2, 64, "bf16", 1, 300, False),        # row-wise, G = 17
-    (600, 8, 2, 256, "bf16", 16, 400, False),       # row-wise, d = 256
+    (600, 8, 2, 256, "bf16", 4, 400, False),        # row-wise, d = 256, b < 16
+    (600, 8, 2, 256, "bf16", 16, 400, False),       # block kernel, d = 256, 7 tiles
+    (2048, 8, 2, 256, "bf16", 64, 1024, False),     # block kernel, d = 256, 16 tiles
+    (2200, 8, 4, 256, "bf16", 16, 700, True),       # block kernel, d = 256, G = 2, shuffled
+    (4200, 4, 2, 256, "bf16", 64, 3000, False),     # block kernel, d = 256, 47 tiles
 ]
 
 
@@ -153,6 +157,9 @@ DENSE_CASES = [
     (1100, 32, 8, 128, "bf16", True),      # rescale after the first key tile
     (900, 8, 2, 64, "bf16", True),
     (700, 4, 2, 64, "f32", True),
+    (333, 8, 1, 256, "bf16", False),       # d = 256: one group of four waves
+    (700, 16, 4, 256, "bf16", False),
+    (1100, 8, 2, 256, "bf16", True),
 ]
 
 

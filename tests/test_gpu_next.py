@@ -298,6 +298,7 @@ def _paged(k, v, ps, seed, extra=3):
 
 @pytest.mark.parametrize("S,Hq,Hkv,d,b,dtype,ps,head_axis", [
     (300, 8, 2, 128, 64, "bf16", 16, 0),
+    (300, 8, 2, 256, 16, "bf16", 16, 1),
     (300, 8, 2, 64, 16, "bf16", 7, 1),
     (257, 8, 4, 128, 1, "bf16", 32, 0),
     (200, 6, 3, 64, 4, "bf16", 1, 1),
@@ -333,6 +334,35 @@ def test_paged_sparse_attention(S, Hq, Hkv, d, b, dtype, ps, head_axis):
     B.sp_sparse_gqa_attn(p, inp.q.cuda(), inp.k.cuda(), inp.v.cuda(), table.cuda(), o_c)
     torch.cuda.synchronize()
     assert torch.equal(o, o_c)
+
+
+@pytest.mark.parametrize("k_", [2048, 2049])
+def test_paged_head_dim_256_long_support(k_):
+    """At head_dim 256 the paged block kernel caches supports of up to 2048
+    entries (its K/V tiles fill most of LDS); a longer support takes the
+    row-wise kernel. Both match the contiguous call, which is held to the
+    oracle on sampled rows of sharp inputs (32 key tiles, rescale after the
+    first)."""
+    S, Hq, Hkv, d, b = 2300, 8, 2, 256, 64
+    say(f"paged d=256 k={k_}")
+    inp = make_inputs(S, Hq, Hkv, d, dtype="bf16", seed=k_, peaked=True, unit_v=True,
+                      k_ramp=8.0)
+    table = make_support(S, b, k_, seed=7, shuffle=True)
+    kp, vp, pt = _paged(inp.k, inp.v, 64, seed=S)
+    p = B.Problem(S, Hq, Hkv, d, topk=k_, block_q=b, dtype="bf16")
+    o = torch.empty(S, Hq, d, dtype=inp.q.dtype, device="cuda")
+    B.sp_sparse_gqa_attn_paged(p, inp.q.cuda(), kp.cuda(), vp.cuda(), pt.cuda(), table.cuda(), o)
+    o_c = torch.empty_like(o)
+    B.sp_sparse_gqa_attn(p, inp.q.cuda(), inp.k.cuda(), inp.v.cuda(), table.cuda(), o_c)
+    torch.cuda.synchronize()
+    rows = np.concatenate([np.arange(r * b, min(r * b + b, S), 9) for r in (0, 17, 33, 35)])
+    ref = oracle.sparse(inp.q, inp.k, inp.v, table, b, rows=rows)
+    ref_abs = oracle.sparse(inp.q, inp.k, inp.v.abs(), table, b, rows=rows)
+    check_attention(o_c.cpu().double().numpy()[rows], ref, ref_abs, "bf16", "contiguous: ")
+    if k_ <= 2048:
+        assert torch.equal(o, o_c)
+    else:   # row-wise (paged) against the block kernel (contiguous)
+        check_attention(o.cpu().double().numpy()[rows], ref, ref_abs, "bf16", "paged: ")
 
 
 # ------------------------------------------------ chunked prefill rows (f3)
