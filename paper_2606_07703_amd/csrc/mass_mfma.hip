@@ -18,8 +18,9 @@
 // is loaded straight into LDS (padded rows); the next tile's loads are issued
 // as soon as the current one is in registers and run under the exponentials.
 //
-// mass_kernel (the other shapes): 16 queries per workgroup on
-// v_mfma_f32_16x16x32_bf16, K staged through registers.
+// mass_kernel (the other shapes, and every shape at head_dim 256, whose
+// 32-key tiles of eight KV heads would not fit LDS twice): 16 queries per
+// workgroup on v_mfma_f32_16x16x32_bf16, K staged through registers.
 //
 // b = 1 stores P rows directly. b > 1 keeps the block aggregate of the key
 // chunk in LDS until it is stored.
@@ -200,7 +201,11 @@ hipError_t launch_h(const Prob &p, const void *q, const void *k, const float *ls
     case 1: return launch_t<D, 1, HKV>(p, q, k, lse, mass, st);
     case 2: return launch_t<D, 2, HKV>(p, q, k, lse, mass, st);
     case 4: return launch_t<D, 4, HKV>(p, q, k, lse, mass, st);
-    default: return launch_t<D, 8, HKV>(p, q, k, lse, mass, st);
+    default:
+      if constexpr (D == 256)
+        return hipErrorInvalidValue;   // not dispatched here
+      else
+        return launch_t<D, 8, HKV>(p, q, k, lse, mass, st);
   }
 }
 
@@ -502,19 +507,22 @@ hipError_t launch32_d(const Prob &p, const void *q, const void *k, const float *
 
 bool mass_mfma_supported(const Prob &p) {
   const int hpw = p.Hq / kNW;
-  return p.dtype == SP_DTYPE_BF16 && (p.d == 64 || p.d == 128) && p.Hq % kNW == 0 &&
-         (hpw == 1 || hpw == 2 || hpw == 4 || hpw == 8) &&
+  // at d = 256 the 16-query kernel holds 32 registers of query operands per
+  // head: up to four heads a wave (Hq <= 32)
+  return p.dtype == SP_DTYPE_BF16 && (p.d == 64 || p.d == 128 || (p.d == 256 && hpw <= 4)) &&
+         p.Hq % kNW == 0 && (hpw == 1 || hpw == 2 || hpw == 4 || hpw == 8) &&
          (p.Hkv == 1 || p.Hkv == 2 || p.Hkv == 4 || p.Hkv == 8) &&
          (p.b == 1 || (p.b % 16 == 0 && p.b <= 1024));
 }
 
 hipError_t launch_mass_mfma(const Prob &p, const void *q, const void *k, const float *lse,
                             float *mass, hipStream_t st) {
-  if (mass32_supported(p)) {
+  if (p.d != 256 && mass32_supported(p)) {
     if (p.d == 64) return launch32_d<64>(p, q, k, lse, mass, st);
     return launch32_d<128>(p, q, k, lse, mass, st);
   }
   if (p.d == 64) return launch_d<64>(p, q, k, lse, mass, st);
+  if (p.d == 256) return launch_d<256>(p, q, k, lse, mass, st);
   return launch_d<128>(p, q, k, lse, mass, st);
 }
 

@@ -63,15 +63,14 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
   // q and o are addressed by position: the host shifts them back by qo rows
   constexpr int KS = D / 32, DT = D / 16;
   constexpr int PPR = D / 8;         // 16-byte pieces per K/V row
-  constexpr int VSTEP = 16 / PPR;    // row stride of a lane's V pieces
-  constexpr int RPL = 8 / VSTEP;     // V pieces per lane per tile
+  constexpr int RPL = PPR / 2;       // V pieces per lane per tile (8 rows x PPR / 16 lanes)
   using Slots = QuerySlots<NW, D>;
   constexpr int VRB = Slots::VRB;
   __shared__ __align__(16) Slots sh;
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int g = lane >> 4, c16 = lane & 15;
-  const int vpiece = c16 % PPR, vsub = c16 / PPR;
+
   const int j = blockIdx.x % Hkv;
   const int grp = n_groups - 1 - blockIdx.x / Hkv;   // longest queries first
   const int t = qo + grp * NW + wave;
@@ -115,10 +114,15 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
     const int ntiles = (last + kQT) / kQT;
     if (ntiles == 0) continue;
 
-    // Gather of tile it: K rows into A operands, V rows into registers. A V
-    // row is PPR 16-byte pieces; lane (g, c16) takes piece c16 % PPR of the
-    // rows 8g + c16 / PPR + (16 / PPR) e, e < RPL (its own 8 entries at d=128).
+    // Gather of tile it: K rows into A operands, V rows into registers. The
+    // 8 V rows of group g are 8 PPR 16-byte pieces; lane (g, c16) takes
+    // pieces c16 + 16e, e < RPL, that is piece (c16 + 16e) % PPR of row
+    // 8g + (c16 + 16e) / PPR (at d = 128 its own 8 entries, whole).
     uint4 kreg[2][KS], vreg[RPL];
+    // tile entry (within the group's 8) and piece of the lane's V piece e:
+    // compile-time where PPR >= 16, else the lane's half picks the entry
+    auto ventry = [&](int e) { return PPR >= 16 ? 16 * e / PPR : (c16 + 16 * e) / PPR; };
+    auto vpiece = [&](int e) { return (c16 + 16 * e) % PPR; };
     auto issue = [&](int it) {
       const int e0 = it * kQT;
 #pragma unroll
@@ -134,9 +138,14 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
       const int ps[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
 #pragma unroll
       for (int e = 0; e < RPL; ++e) {
-        // entry 8g + vsub + VSTEP e (vsub is 0 when VSTEP is 1)
-        const int s = max(vsub ? ps[VSTEP * e + VSTEP - 1] : ps[VSTEP * e], 0);
-        vreg[e] = ldg16(v + (size_t)s * kv_row + kv_head + vpiece * 8);
+        int s;
+        if constexpr (PPR >= 16) {
+          s = ps[16 * e / PPR];
+        } else {   // entries 2e (lanes c16 < 8) and 2e + 1 (c16 >= 8) at d = 64
+          static_assert(PPR == 8, "d = 64, 128 or 256");
+          s = c16 >= 8 ? ps[2 * e + 1] : ps[2 * e];
+        }
+        vreg[e] = ldg16(v + (size_t)max(s, 0) * kv_row + kv_head + vpiece(e) * 8);
       }
     };
     issue(0);
@@ -144,7 +153,7 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
       // V rows of this tile -> wave slot (after the previous tile's reads)
 #pragma unroll
       for (int e = 0; e < RPL; ++e)
-        sts16(vb + (8 * g + vsub + VSTEP * e) * VRB + vpiece * 16, vreg[e]);
+        sts16(vb + (8 * g + ventry(e)) * VRB + vpiece(e) * 16, vreg[e]);
       f32x4 sacc[2];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
@@ -226,7 +235,9 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
 template <int D>
 hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
                     const int32_t *idx, void *o, hipStream_t st, KvPages pages) {
-  constexpr int NW = 4;
+  // waves are independent; at d = 256 two per workgroup keep three
+  // workgroups' LDS slots on a CU
+  constexpr int NW = D == 256 ? 2 : 4;
   const int n_groups = (p.nq + NW - 1) / NW;
   const size_t shift = (size_t)p.qo * p.Hq * D;   // chunk rows addressed by position
   hipLaunchKernelGGL((sparse_query_kernel<D, NW>), dim3(n_groups * p.Hkv), dim3(NW * 64), 0, st,
@@ -240,12 +251,13 @@ hipError_t launch_d(const Prob &p, const void *q, const void *k, const void *v,
 }  // namespace
 
 bool sparse_query_mfma_supported(const Prob &p) {
-  return p.dtype == SP_DTYPE_BF16 && (p.d == 64 || p.d == 128) && p.G <= 16;
+  return p.dtype == SP_DTYPE_BF16 && (p.d == 64 || p.d == 128 || p.d == 256) && p.G <= 16;
 }
 
 hipError_t launch_sparse_query_mfma(const Prob &p, const void *q, const void *k, const void *v,
                                     const int32_t *idx, void *o, hipStream_t st, KvPages pages) {
   if (p.d == 64) return launch_d<64>(p, q, k, v, idx, o, st, pages);
+  if (p.d == 256) return launch_d<256>(p, q, k, v, idx, o, st, pages);
   return launch_d<128>(p, q, k, v, idx, o, st, pages);
 }
 

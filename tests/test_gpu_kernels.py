@@ -53,6 +53,7 @@ SPARSE_CASES = [
     (300, 32, 2, 64, "bf16", 1, 100),      # G = 16: every MFMA column a head
     (400, 12, 4, 128, "bf16", 1, 33),      # G = 3, ragged last tile
     (260, 4, 1, 64, "bf16", 3, 2100),      # support row longer than one LDS chunk
+    (260, 8, 2, 256, "bf16", 1, 2100),     # the same at d = 256
     (130, 34, 2, 64, "bf16", 1, 40),       # G = 17: row-wise path
 ]
 
@@ -84,7 +85,9 @@ SHARP_CASES = [
     (1500, 8, 2, 64, "bf16", 4, 700, True),         # per-query kernel, b = 4, shuffled
     (1200, 4, 2, 64, "f32", 1, 500, False),         # row-wise, fp32
     (700, 34, 2, 64, "bf16", 1, 300, False),        # row-wise, G = 17
-    (600, 8, 2, 256, "bf16", 4, 400, False),        # row-wise, d = 256, b < 16
+    (600, 8, 2, 256, "bf16", 4, 400, False),        # per-query kernel, d = 256, b = 4
+    (1500, 8, 2, 256, "bf16", 1, 700, True),        # per-query kernel, d = 256, shuffled
+    (700, 34, 2, 256, "bf16", 1, 300, False),       # row-wise, d = 256, G = 17
     (600, 8, 2, 256, "bf16", 16, 400, False),       # block kernel, d = 256, 7 tiles
     (2048, 8, 2, 256, "bf16", 64, 1024, False),     # block kernel, d = 256, 16 tiles
     (2200, 8, 4, 256, "bf16", 16, 700, True),       # block kernel, d = 256, G = 2, shuffled
@@ -279,6 +282,10 @@ MASS_CASES = [
     (300, 16, 4, 64, 32, "sum", "bf16"),
     (1000, 32, 8, 128, 128, "max", "bf16"),
     (200, 8, 1, 64, 1, "max", "bf16"),
+    (300, 8, 2, 256, 1, "max", "bf16"),    # d = 256: the 16-query kernel
+    (700, 32, 8, 256, 64, "max", "bf16"),
+    (500, 16, 4, 256, 16, "sum", "bf16"),
+    (300, 12, 4, 256, 32, "max", "bf16"),  # Hq not a multiple of 8: row-wise
 ]
 
 
