@@ -57,7 +57,8 @@ HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 FP32_VALU_PEAK_TFLOPS = 157.3
 METRIC = "ms/layer sparse GQA prefill @32K, speedup vs own dense, % HBM/MFMA roofline"
-ALL_WORKLOADS = ("oracle_tiny_512", "indexer_4k", "block_16k", "headline_32k", "stress_100k")
+ALL_WORKLOADS = ("oracle_tiny_512", "indexer_4k", "block_16k", "headline_32k", "stress_100k",
+                 "head256_32k")
 
 
 def causal_pairs(S: int) -> int:
@@ -211,6 +212,10 @@ def build_plan(w, dev, B, PL, make_inputs, make_projection_inputs):
         indexer_mode("block64max", 64, agg="max", W=w.local_window)
         dense()
         plan.value_mode = "block64sum"
+    elif w.name == "head256_32k":
+        indexer_mode("block64", 64, paged=True)
+        dense()
+        plan.value_mode = "block64"
     elif w.name == "stress_100k":
         b = w.block_q[0]
         indexer_mode(f"block{b}", b)
@@ -589,7 +594,8 @@ def write_summary(args, lines):
         cpu = d["cpu_baseline"]
         cpu_s = "—" if not cpu else (f"{cpu['value']} ({cpu['cores']}); " + ", ".join(
             f"{k} {v['ms_per_layer']}" for k, v in cpu["legs"].items()))
-        L.append(f"| {cfg['workload']} (S={cfg['seq_len']}, b={cfg['block_q']}, k={cfg['topk']}) "
+        L.append(f"| {cfg['workload']} (S={cfg['seq_len']}, d={cfg['head_dim']}, b={cfg['block_q']}, "
+                 f"k={cfg['topk']}) "
                  f"| {cfg['selection']} | {d['value']} | {d['dense_ms']} | {d['speedup_vs_dense']} "
                  f"| {others or '—'} | {r['kernel']}: {r['frac']} of {r['peak']} {r['unit']} "
                  f"| {cpu_s} |")

@@ -68,6 +68,14 @@ WORKLOADS = {
         modes=("indexer", "dense"), seed=5,
         description="S=102400, 32/8 heads, d=128, d_idx=128, top-4096 per 128-query block, "
                     "256 stratified needles, plus an untrained-indexer variant"),
+    # not one of the paper's measured configurations: the 32K shape at the
+    # head dim of the paper's Qwen3.5 models (Section 6.3: d_idx = 256 equals
+    # it), timing the head_dim-256 kernels
+    "head256_32k": Workload(
+        name="head256_32k", seq_len=32768, num_q_heads=32, num_kv_heads=8,
+        head_dim=256, index_dim=256, topk=2048, block_q=(64,), local_window=0,
+        agg=("max",), dtype="bf16", needles=128, modes=("indexer", "dense"), seed=6,
+        description="S=32768, 32/8 heads, d=256, d_idx=256, top-2048 per 64-query block"),
 }
 
 

@@ -193,6 +193,7 @@ WORKLOAD_CASES = [
     ("headline_32k", 1, "max", False),
     ("stress_100k", 128, "max", False),
     ("stress_100k", 128, "max", True),
+    ("head256_32k", 64, "max", False),
 ]
 
 
@@ -215,7 +216,7 @@ def test_workload_indexer_mode(name, b, agg, untrained):
                    want_needles=not untrained)
 
 
-@pytest.mark.parametrize("name", ["indexer_4k", "headline_32k"])
+@pytest.mark.parametrize("name", ["indexer_4k", "headline_32k", "head256_32k"])
 def test_workload_dense_sampled(name):
     w = get_workload(name)
     say(f"dense workload {name}")
@@ -254,7 +255,7 @@ def test_workload_oracle_mode_headline_sampled():
 
 
 FULL_SIZE_SPARSE = [("headline_32k", 64), ("headline_32k", 1), ("block_16k", 64),
-                    ("stress_100k", 128)]
+                    ("stress_100k", 128), ("head256_32k", 64)]
 
 
 @pytest.mark.parametrize("variant", ["workload", "sharp"])
