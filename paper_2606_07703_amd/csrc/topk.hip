@@ -63,13 +63,14 @@ __device__ __forceinline__ uint32_t scan_bits(uint32_t v, uint32_t (*scratch)[NT
 }
 
 // Given NC interleaved copies of a filled histogram of nb bins (bin i of
-// copy c at hist[i*NC + c]), find the bin holding the `remaining`-th largest
-// key; writes (bin, rank within bin) to sel. Every thread must call it (it
-// contains barriers).
-template <int NT, int NC = 1>
+// copy c at hist[i*NC + c]), less sub0 in bin 0, find the bin holding the
+// `remaining`-th largest key; writes (bin, rank within bin) to sel. CMASK
+// covers the bits of a thread's count (the keys of its bins). Every thread
+// must call it (it contains barriers).
+template <int NT, uint32_t CMASK, int NC = 1>
 __device__ __forceinline__ void find_digit(const uint32_t *hist, int nb, uint32_t remaining,
                                            uint32_t (*scratch)[NT / 64], int row,
-                                           uint32_t *sel) {
+                                           uint32_t *sel, uint32_t sub0 = 0) {
   const int tid = threadIdx.x;
   const int per = nb / NT;            // nb is a multiple of NT
   const int hi = nb - tid * per;      // thread 0 owns the highest bins
@@ -77,12 +78,12 @@ __device__ __forceinline__ void find_digit(const uint32_t *hist, int nb, uint32_
     uint32_t c = 0;
 #pragma unroll
     for (int x = 0; x < NC; ++x) c += hist[i * NC + x];
-    return c;
+    return i == 0 ? c - sub0 : c;
   };
   uint32_t mine = 0;
   for (int i = hi - per; i < hi; ++i) mine += bin(i);
   uint32_t total;
-  const uint32_t above = scan_bits<NT, 0xffffu>(mine, scratch, row, &total);
+  const uint32_t above = scan_bits<NT, CMASK>(mine, scratch, row, &total);
   if (above < remaining && above + mine >= remaining) {
     uint32_t acc = above;
     for (int i = hi - 1; i >= hi - per; --i) {
@@ -98,6 +99,16 @@ __device__ __forceinline__ void find_digit(const uint32_t *hist, int nb, uint32_
   __syncthreads();
 }
 
+// Row of workgroup i of n. Row r has (r + 1) b candidates, so the first half
+// of the grid takes the rows from the longest down and the second half from
+// the shortest up: workgroups i and i + n/2, which the dispatcher places on
+// one CU when the grid is two workgroups per CU, then hold rows of equal
+// total length, and a longer grid starts its longest rows first.
+__device__ __forceinline__ int row_of(int i, int n) {
+  const int half = (n + 1) / 2;
+  return i < half ? n - 1 - i : i - half;
+}
+
 // ------------------------------------------------------------ register rows
 constexpr int kRegNT = 512;
 constexpr int kRun = 16;                      // consecutive positions per run
@@ -110,15 +121,21 @@ constexpr int kRegCap = kRegNT * kRun * kRegSub;   // 32768 candidates
 // spread out and use one copy.
 constexpr int kCopies = 4;
 
-__global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int qo, int b, int k, int W,
-                                                          const float *__restrict__ scores,
-                                                          int32_t *__restrict__ idx) {
+// Two workgroups per CU (16 waves: at most 128 registers a wave), so that a
+// long row and a short one share each CU (see row_of).
+__global__ __launch_bounds__(kRegNT) __attribute__((amdgpu_waves_per_eu(4, 4))) void
+topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ scores,
+                int32_t *__restrict__ idx) {
   constexpr int NT = kRegNT;
-  __shared__ uint32_t hist[kCopies * 2048];
+  constexpr int kHist = kCopies * 2048;
+  // histogram copies, then one discard word per lane (counts of keys outside
+  // the digit's prefix go there, so every key costs one unconditional
+  // atomic and no branch); after the passes, the output row is staged here
+  __shared__ uint32_t hist[kHist + 64];
   __shared__ uint32_t scratch[2][NT / 64];
   __shared__ uint32_t sel[2];
 
-  const int r = blockIdx.x;
+  const int r = row_of((int)blockIdx.x, (int)gridDim.x);
   const int tid = threadIdx.x, lane = tid & 63;
   const int t1 = min(qo + r * b + b, S) - 1;   // rows count blocks from the chunk start
   const int L = t1 + 1;
@@ -136,7 +153,12 @@ __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int qo, int b, 
   const int nsub = (nc + NT * kRun - 1) / (NT * kRun);   // runs in use (<= kRegSub)
   const bool vec = (((row_id * S) & 3) == 0);            // row start 16-byte aligned
 
-  // Run j of thread t covers positions [kRun*(t + NT*j), +kRun).
+  // Run j of thread t covers positions [kRun*(t + NT*j), +kRun). Positions
+  // at or past nc hold key 0 (kPadKey), which lands in bin 0 of a digit
+  // while every digit fixed so far is 0; those npad keys are taken out of
+  // that bin's count.
+  constexpr uint32_t kPadKey = 0u;
+  const uint32_t npad = (uint32_t)(nsub * NT * kRun - nc);
   uint32_t key[kRegSub][kRun];
 #pragma unroll
   for (int j = 0; j < kRegSub; ++j) {
@@ -155,7 +177,7 @@ __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int qo, int b, 
         }
       }
 #pragma unroll
-      for (int e = 0; e < 4; ++e) key[j][i + e] = float_key(f[e]);
+      for (int e = 0; e < 4; ++e) key[j][i + e] = p0 + i + e < nc ? float_key(f[e]) : kPadKey;
     }
   }
 
@@ -163,6 +185,7 @@ __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int qo, int b, 
   if (kp > 0) {
     uint32_t prefix = 0, pmask = 0;
     remaining = (uint32_t)kp;
+    uint32_t *discard = hist + kHist + lane;
 #pragma unroll 1
     for (int pass = 0; pass < 3; ++pass) {
       const int shift = digit_shift(pass), nb = 1 << digit_bits(pass);
@@ -172,17 +195,20 @@ __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int qo, int b, 
       for (int i = tid; i < nb * nco; i += NT) hist[i] = 0;
       __syncthreads();
       uint32_t zc = 0;
+      // opaque to the compiler, so the per-key zero tests stay inside the
+      // pass instead of being hoisted out as 64 saved lane masks
+      uint32_t zkey = kZeroKey;
+      asm volatile("" : "+s"(zkey));
 #pragma unroll
       for (int j = 0; j < kRegSub; ++j) {
-        if (j >= nsub) continue;
-        const int p0 = kRun * (tid + NT * j);
+        if (j >= nsub) continue;   // uniform
 #pragma unroll
         for (int i = 0; i < kRun; ++i) {
           const uint32_t kv = key[j][i];
-          if (p0 + i < nc && (kv & pmask) == prefix) {
-            if (kv == kZeroKey) ++zc;
-            else atomicAdd(&hc[((kv >> shift) & dmask) * nco], 1u);
-          }
+          const bool in = (kv & pmask) == prefix;
+          const bool zero = kv == zkey;
+          zc += (in && zero) ? 1u : 0u;
+          atomicAdd(in && !zero ? &hc[((kv >> shift) & dmask) * nco] : discard, 1u);
         }
       }
       if ((kZeroKey & pmask) == prefix) {
@@ -191,10 +217,11 @@ __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int qo, int b, 
         if (lane == 0 && zc) atomicAdd(&hist[((kZeroKey >> shift) & dmask) * nco], zc);
       }
       __syncthreads();
+      const uint32_t sub0 = prefix == 0 ? npad : 0u;
       if (pass == 0)
-        find_digit<NT, kCopies>(hist, nb, remaining, scratch, 0, sel);
+        find_digit<NT, 0xffffu, kCopies>(hist, nb, remaining, scratch, 0, sel, sub0);
       else
-        find_digit<NT>(hist, nb, remaining, scratch, pass & 1, sel);
+        find_digit<NT, 0xffffu>(hist, nb, remaining, scratch, pass & 1, sel, sub0);
       prefix |= sel[0] << shift;
       pmask |= dmask << shift;
       remaining = sel[1];
@@ -204,43 +231,61 @@ __global__ __launch_bounds__(kRegNT) void topk_reg_kernel(int S, int qo, int b, 
   }
 
   // Ordered emission, one run index j at a time (runs of index j, in thread
-  // order, cover positions [kRun*NT*j, kRun*NT*(j+1)) in order).
-  uint32_t gt_before = 0, eq_before = 0;
+  // order, cover positions [kRun*NT*j, kRun*NT*(j+1)) in order). Chosen
+  // positions are written to their output slot in LDS (hist, free after the
+  // passes) when the row fits, then copied out with coalesced stores.
+  auto emit = [&](auto staged_tag) {
+    constexpr bool STAGED = decltype(staged_tag)::value;
+    uint32_t gt_before = 0, eq_before = 0;
 #pragma unroll
-  for (int j = 0; j < kRegSub; ++j) {
-    if (j >= nsub) break;   // uniform
-    const int p0 = kRun * (tid + NT * j);
-    uint32_t cgt = 0, ceq = 0;
+    for (int j = 0; j < kRegSub; ++j) {
+      if (j >= nsub) break;   // uniform
+      const int p0 = kRun * (tid + NT * j);
+      const int nv = min(max(nc - p0, 0), kRun);   // this run's real positions
+      uint32_t cgt = 0, ceq = 0;
 #pragma unroll
-    for (int i = 0; i < kRun; ++i) {
-      if (p0 + i < nc) {
-        cgt += key[j][i] > T;
-        ceq += key[j][i] == T;
+      for (int i = 0; i < kRun; ++i) {
+        cgt += (i < nv && key[j][i] > T) ? 1u : 0u;
+        ceq += (i < nv && key[j][i] == T) ? 1u : 0u;
       }
-    }
-    uint32_t total;
-    // counts of at most 16 each: bits 0..4 and 16..20
-    const uint32_t ex = scan_bits<NT, 0x1f001fu>((cgt << 16) | ceq, scratch, (j + 1) & 1, &total);
-    const uint32_t my_gt = gt_before + (ex >> 16);
-    uint32_t my_eq = eq_before + (ex & 0xffffu);
-    uint32_t pos = my_gt + min(my_eq, remaining);
+      uint32_t total;
+      // counts of at most 16 each: bits 0..4 and 16..20
+      const uint32_t ex =
+          scan_bits<NT, 0x1f001fu>((cgt << 16) | ceq, scratch, (j + 1) & 1, &total);
+      const uint32_t my_gt = gt_before + (ex >> 16);
+      uint32_t my_eq = eq_before + (ex & 0xffffu);
+      uint32_t pos = my_gt + min(my_eq, remaining);
+      // fresh, opaque copies: the compares below are not shared with the
+      // counting loop above, whose lane masks would otherwise all stay live
+      uint32_t Tc = T;
+      int nvc = nv, p0c = p0;
+      asm volatile("" : "+v"(Tc));
+      asm volatile("" : "+v"(nvc));
+      asm volatile("" : "+v"(p0c));   // positions recomputed here, not kept from the loads
 #pragma unroll
-    for (int i = 0; i < kRun; ++i) {
-      if (p0 + i < nc) {
+      for (int i = 0; i < kRun; ++i) {
         const uint32_t kv = key[j][i];
-        bool take = kv > T;
-        if (kv == T) {
-          take = my_eq < remaining;
-          ++my_eq;
+        const bool eq = i < nvc && kv == Tc;
+        const bool take = (i < nvc && kv > Tc) || (eq && my_eq < remaining);
+        my_eq += eq ? 1u : 0u;
+        if constexpr (STAGED) {
+          // unchosen positions go to the lane's discard word: no branch
+          hist[take ? pos : (uint32_t)(kHist + lane)] = (uint32_t)(p0c + i);
+        } else {
+          if (take && pos < (uint32_t)kp) out[pos] = p0c + i;   // pos < kp always holds
         }
-        if (take) {
-          if (pos < (uint32_t)kp) out[pos] = p0 + i;   // always true for consistent counts
-          ++pos;
-        }
+        pos += take ? 1u : 0u;
       }
+      gt_before += total >> 16;
+      eq_before += total & 0xffffu;
     }
-    gt_before += total >> 16;
-    eq_before += total & 0xffffu;
+  };
+  if (kp <= kHist) {
+    emit(std::true_type{});
+    __syncthreads();
+    for (int c = tid; c < kp; c += NT) out[c] = (int32_t)hist[c];
+  } else {
+    emit(std::false_type{});
   }
   for (int c = tid; c < Wf; c += NT) out[kp + c] = nc + c;
 }
@@ -259,7 +304,7 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, in
   __shared__ uint32_t sel[2];
   __shared__ uint32_t keys[kEmitPer * kEmitStride];
 
-  const int r = blockIdx.x;
+  const int r = row_of((int)blockIdx.x, (int)gridDim.x);
   const int tid = threadIdx.x, lane = tid & 63;
   const int t1 = min(qo + r * b + b, S) - 1;   // rows count blocks from the chunk start
   const int L = t1 + 1;
@@ -301,7 +346,8 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, in
         if (lane == 0 && zc) atomicAdd(&hist[(kZeroKey >> shift) & dmask], zc);
       }
       __syncthreads();
-      find_digit<kNT>(hist, nb, remaining, scratch, pass & 1, sel);
+      // a thread's bins can hold more than 65535 of a long row's keys
+      find_digit<kNT, 0xffffffffu>(hist, nb, remaining, scratch, pass & 1, sel);
       prefix |= sel[0] << shift;
       pmask |= dmask << shift;
       remaining = sel[1];
