@@ -238,6 +238,25 @@ def test_topk(case):
     assert np.array_equal(got, ref)   # same fp32 values: selection must be bit-exact
 
 
+def test_topk_streamed_crowded_bins():
+    """A streamed row (70000 candidates) whose top bins hold 66000 equal keys
+    and whose k-th largest lies below them: the block scan of per-thread bin
+    counts must carry counts above 65535 to the threads owning lower bins."""
+    S, k = 70000, 68000
+    say("topk streamed crowded bins")
+    rng = np.random.default_rng(11)
+    row = np.ones(S, dtype=np.float32)
+    low = rng.choice(S, 4000, replace=False)
+    row[low] = -1.0 - rng.random(4000).astype(np.float32)
+    scores = torch.from_numpy(row[None, :].copy())
+    p = B.Problem(S, 1, 1, 64, topk=k, block_q=S, dtype="f32")
+    idx = torch.empty(1, k, dtype=torch.int32, device="cuda")
+    B.sp_topk_select(p, cuda(scores), idx)
+    torch.cuda.synchronize()
+    ref = oracle.topk(scores.numpy().astype(np.float64), np.array([S]), k, 0)
+    assert np.array_equal(idx.cpu().numpy(), ref)
+
+
 # --------------------------------------------------------------- indexer scores
 INDEXER_CASES = [
     # S, d_idx, b, agg, relu, dtype
