@@ -586,10 +586,8 @@ __device__ __forceinline__ void attn_finish(const AttnState<D> &st, const QRow<D
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         uint2 w;
-        w.x = (uint32_t)float_to_bf16(st.o[dt][4 * i] * inv) |
-              ((uint32_t)float_to_bf16(st.o[dt][4 * i + 1] * inv) << 16);
-        w.y = (uint32_t)float_to_bf16(st.o[dt][4 * i + 2] * inv) |
-              ((uint32_t)float_to_bf16(st.o[dt][4 * i + 3] * inv) << 16);
+        w.x = pack_bf16x2(st.o[dt][4 * i] * inv, st.o[dt][4 * i + 1] * inv);
+        w.y = pack_bf16x2(st.o[dt][4 * i + 2] * inv, st.o[dt][4 * i + 3] * inv);
         *reinterpret_cast<uint2 *>(op + 32 * dt + 8 * i) = w;
       }
   }

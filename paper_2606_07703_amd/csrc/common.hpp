@@ -30,6 +30,14 @@ __device__ __forceinline__ float bf16_to_float(uint16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
+// Two floats -> two bf16 in one word (a low, b high), round to nearest even,
+// by the hardware packed conversion.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
 // Round-to-nearest-even float -> bf16 (NaN kept quiet).
 __device__ __forceinline__ uint16_t float_to_bf16(float f) {
   uint32_t x = __float_as_uint(f);

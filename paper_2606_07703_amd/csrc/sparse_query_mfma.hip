@@ -224,10 +224,8 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) {
     uint2 w;
-    w.x = (uint32_t)float_to_bf16(oacc[dt][0] * inv) |
-          ((uint32_t)float_to_bf16(oacc[dt][1] * inv) << 16);
-    w.y = (uint32_t)float_to_bf16(oacc[dt][2] * inv) |
-          ((uint32_t)float_to_bf16(oacc[dt][3] * inv) << 16);
+    w.x = pack_bf16x2(oacc[dt][0] * inv, oacc[dt][1] * inv);
+    w.y = pack_bf16x2(oacc[dt][2] * inv, oacc[dt][3] * inv);
     *reinterpret_cast<uint2 *>(op + dt * 16 + g * 4) = w;
   }
 }

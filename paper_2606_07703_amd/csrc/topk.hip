@@ -242,39 +242,44 @@ topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ sc
       if (j >= nsub) break;   // uniform
       const int p0 = kRun * (tid + NT * j);
       const int nv = min(max(nc - p0, 0), kRun);   // this run's real positions
-      uint32_t cgt = 0, ceq = 0;
+      // bit i: key i of the run is above T / equal to T
+      uint32_t gtm = 0, eqm = 0;
 #pragma unroll
       for (int i = 0; i < kRun; ++i) {
-        cgt += (i < nv && key[j][i] > T) ? 1u : 0u;
-        ceq += (i < nv && key[j][i] == T) ? 1u : 0u;
+        gtm |= key[j][i] > T ? 1u << i : 0u;
+        eqm |= key[j][i] == T ? 1u << i : 0u;
       }
+      const uint32_t vmask = (1u << nv) - 1u;   // nv <= 16
+      gtm &= vmask;
+      eqm &= vmask;
+      const uint32_t cgt = (uint32_t)__popc(gtm), ceq = (uint32_t)__popc(eqm);
       uint32_t total;
       // counts of at most 16 each: bits 0..4 and 16..20
       const uint32_t ex =
           scan_bits<NT, 0x1f001fu>((cgt << 16) | ceq, scratch, (j + 1) & 1, &total);
       const uint32_t my_gt = gt_before + (ex >> 16);
-      uint32_t my_eq = eq_before + (ex & 0xffffu);
-      uint32_t pos = my_gt + min(my_eq, remaining);
-      // fresh, opaque copies: the compares below are not shared with the
-      // counting loop above, whose lane masks would otherwise all stay live
-      uint32_t Tc = T;
-      int nvc = nv, p0c = p0;
-      asm volatile("" : "+v"(Tc));
-      asm volatile("" : "+v"(nvc));
-      asm volatile("" : "+v"(p0c));   // positions recomputed here, not kept from the loads
-#pragma unroll
-      for (int i = 0; i < kRun; ++i) {
-        const uint32_t kv = key[j][i];
-        const bool eq = i < nvc && kv == Tc;
-        const bool take = (i < nvc && kv > Tc) || (eq && my_eq < remaining);
-        my_eq += eq ? 1u : 0u;
-        if constexpr (STAGED) {
-          // unchosen positions go to the lane's discard word: no branch
-          hist[take ? pos : (uint32_t)(kHist + lane)] = (uint32_t)(p0c + i);
-        } else {
-          if (take && pos < (uint32_t)kp) out[pos] = p0c + i;   // pos < kp always holds
-        }
-        pos += take ? 1u : 0u;
+      const uint32_t my_eq = eq_before + (ex & 0xffffu);
+      // chosen: every key above T, and the first (remaining - my_eq) of the
+      // run's keys equal to T (none once my_eq reaches remaining; written
+      // without a wrapping subtraction)
+      const uint32_t used = min(my_eq, remaining);
+      uint32_t neq = min(remaining - used, ceq);
+      uint32_t take = gtm, e = eqm;
+      for (; neq > 0; --neq) {
+        const uint32_t low = e & (0u - e);
+        take |= low;
+        e ^= low;
+      }
+      // chosen positions in order, from this run's first output slot
+      uint32_t pos = my_gt + used;
+      while (take) {
+        const int i = __builtin_ctz(take);
+        take &= take - 1u;
+        if constexpr (STAGED)
+          hist[pos] = (uint32_t)(p0 + i);
+        else if (pos < (uint32_t)kp)   // always true for consistent counts
+          out[pos] = p0 + i;
+        ++pos;
       }
       gt_before += total >> 16;
       eq_before += total & 0xffffu;
