@@ -95,8 +95,7 @@ typedef struct sp_problem {
   int32_t num_q_heads;  /* Hq >= 1, a multiple of num_kv_heads */
   int32_t num_kv_heads; /* Hkv >= 1 */
   int32_t head_dim;     /* d: 64, 128 or 256 (Section 6.3: d = d_idx = 256
-                           for some backbones; 256 runs on the row-wise
-                           kernels) */
+                           for some backbones) */
   int32_t index_dim;    /* d_idx: 64, 128 or 256 (indexer calls only) */
   int32_t topk;         /* k >= 1; k >= t1_r+1 keeps every causal key */
   int32_t block_q;      /* b >= 1; 1 = per-query support */
