@@ -92,6 +92,7 @@ SHARP_CASES = [
     (2048, 8, 2, 256, "bf16", 64, 1024, False),     # block kernel, d = 256, 16 tiles
     (2200, 8, 4, 256, "bf16", 16, 700, True),       # block kernel, d = 256, G = 2, shuffled
     (4200, 4, 2, 256, "bf16", 64, 3000, False),     # block kernel, d = 256, 47 tiles
+    (4700, 4, 2, 64, "bf16", 64, 4500, True),       # b = 64 with k > 4096: per-query kernel
 ]
 
 
