@@ -40,8 +40,11 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 template <int NW, int D>
 struct QuerySlots {
   static constexpr int VRB = 2 * D + 32;   // V row bytes: conflict-free transpose reads
+  static constexpr int KRB = 2 * D + 16;   // K row bytes: conflict-free operand reads
   int pos[NW][kPosChunk];
-  char vbuf[NW][kQT * VRB];
+  // one slot per wave: a tile's K rows, then (once its products have read
+  // them) the same tile's V rows
+  char slot[NW][kQT * (VRB > KRB ? VRB : KRB)];
 };
 
 template <class Op>
@@ -65,7 +68,7 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
   constexpr int PPR = D / 8;         // 16-byte pieces per K/V row
   constexpr int RPL = PPR / 2;       // V pieces per lane per tile (8 rows x PPR / 16 lanes)
   using Slots = QuerySlots<NW, D>;
-  constexpr int VRB = Slots::VRB;
+  constexpr int VRB = Slots::VRB, KRB = Slots::KRB;
   __shared__ __align__(16) Slots sh;
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -77,7 +80,8 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
   if (t >= S) return;   // no workgroup barrier below: waves are independent
   const int32_t *row = idx + (size_t)j * gstride + (size_t)((t - qo) / b) * kk;
   int *ipos = sh.pos[wave];
-  char *vb = sh.vbuf[wave];
+  char *vb = sh.slot[wave];
+  char *kbs = sh.slot[wave];
 
   // Q as the B operand of S^T = K Q^T: column c16 is head j*G + c16.
   const bool hcol = c16 < G;
@@ -114,25 +118,20 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
     const int ntiles = (last + kQT) / kQT;
     if (ntiles == 0) continue;
 
-    // Gather of tile it: K rows into A operands, V rows into registers. The
-    // 8 V rows of group g are 8 PPR 16-byte pieces; lane (g, c16) takes
-    // pieces c16 + 16e, e < RPL, that is piece (c16 + 16e) % PPR of row
-    // 8g + (c16 + 16e) / PPR (at d = 128 its own 8 entries, whole).
-    uint4 kreg[2][KS], vreg[RPL];
+    // Gather of tile it into registers, K and V alike: the 8 rows of group g
+    // are 8 PPR 16-byte pieces; lane (g, c16) takes pieces c16 + 16e, e <
+    // RPL, that is piece (c16 + 16e) % PPR of row 8g + (c16 + 16e) / PPR (at
+    // d = 128 its own 8 entries, whole). A gather instruction then covers 4
+    // whole rows: the address unit serves that shape at more than twice the
+    // rate of 16 rows x 64 bytes (the MFMA operand layout, which K is read
+    // in from the wave's LDS slot instead).
+    uint4 kreg[RPL], vreg[RPL];
     // tile entry (within the group's 8) and piece of the lane's V piece e:
     // compile-time where PPR >= 16, else the lane's half picks the entry
     auto ventry = [&](int e) { return PPR >= 16 ? 16 * e / PPR : (c16 + 16 * e) / PPR; };
     auto vpiece = [&](int e) { return (c16 + 16 * e) % PPR; };
     auto issue = [&](int it) {
       const int e0 = it * kQT;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        int s = ipos[e0 + 8 * (c16 >> 2) + 4 * kt + (c16 & 3)];
-        s = max(s, 0);
-        const uint16_t *kp = k + (size_t)s * kv_row + kv_head + g * 8;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) kreg[kt][ks] = ldg16(kp + ks * 32);
-      }
       const int4 pa = *reinterpret_cast<const int4 *>(ipos + e0 + 8 * g);
       const int4 pb = *reinterpret_cast<const int4 *>(ipos + e0 + 8 * g + 4);
       const int ps[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
@@ -145,22 +144,33 @@ __global__ __launch_bounds__(NW * 64) void sparse_query_kernel(
           static_assert(PPR == 8, "d = 64, 128 or 256");
           s = c16 >= 8 ? ps[2 * e + 1] : ps[2 * e];
         }
-        vreg[e] = ldg16(v + (size_t)max(s, 0) * kv_row + kv_head + vpiece(e) * 8);
+        const size_t rb = (size_t)max(s, 0) * kv_row + kv_head + vpiece(e) * 8;
+        kreg[e] = ldg16(k + rb);
+        vreg[e] = ldg16(v + rb);
       }
     };
     issue(0);
     for (int it = 0; it < ntiles; ++it) {
-      // V rows of this tile -> wave slot (after the previous tile's reads)
+      // K rows of this tile -> the wave's slot (after the previous tile's V
+      // reads), products S^T = K Q^T, then V rows over them
 #pragma unroll
       for (int e = 0; e < RPL; ++e)
-        sts16(vb + (8 * g + ventry(e)) * VRB + vpiece(e) * 16, vreg[e]);
+        sts16(kbs + (8 * g + ventry(e)) * KRB + vpiece(e) * 16, kreg[e]);
       f32x4 sacc[2];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
         sacc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // A operand: MFMA row c16 of key-tile kt is tile entry 8(c16/4) + 4kt + c16%4
+        const char *krow = kbs + (8 * (c16 >> 2) + 4 * kt + (c16 & 3)) * KRB + g * 16;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) sacc[kt] = mfma16(as_bf16x8(kreg[kt][ks]), qb[ks], sacc[kt]);
+        for (int ks = 0; ks < KS; ++ks)
+          sacc[kt] = mfma16(as_bf16x8(lds16(krow + ks * 64)), qb[ks], sacc[kt]);
       }
+      // the K operand reads have returned (the products consumed them); LDS
+      // operations of one wave complete in order
+#pragma unroll
+      for (int e = 0; e < RPL; ++e)
+        sts16(vb + (8 * g + ventry(e)) * VRB + vpiece(e) * 16, vreg[e]);
       const int e0 = it * kQT;
       const int4 pa = *reinterpret_cast<const int4 *>(ipos + e0 + 8 * g);
       const int4 pb = *reinterpret_cast<const int4 *>(ipos + e0 + 8 * g + 4);
