@@ -26,6 +26,8 @@ namespace sp {
 namespace {
 
 constexpr uint32_t kZeroKey = 0x80000000u;   // float_key(+0.0f)
+// Word 3 of a raw buffer resource on gfx950: 32-bit data format, no swizzle.
+constexpr int kTopkBufferDword3 = 0x00020000;
 
 __device__ __forceinline__ int digit_shift(int pass) { return pass == 0 ? 21 : (pass == 1 ? 10 : 0); }
 __device__ __forceinline__ int digit_bits(int pass) { return pass == 2 ? 10 : 11; }
@@ -63,14 +65,14 @@ __device__ __forceinline__ uint32_t scan_bits(uint32_t v, uint32_t (*scratch)[NT
 }
 
 // Given NC interleaved copies of a filled histogram of nb bins (bin i of
-// copy c at hist[i*NC + c]), less sub0 in bin 0, find the bin holding the
-// `remaining`-th largest key; writes (bin, rank within bin) to sel. CMASK
-// covers the bits of a thread's count (the keys of its bins). Every thread
-// must call it (it contains barriers).
+// copy c at hist[i*NC + c]), less subcnt in bin subbin (padding keys counted
+// there), find the bin holding the `remaining`-th largest key; writes (bin,
+// rank within bin) to sel. CMASK covers the bits of a thread's count (the
+// keys of its bins). Every thread must call it (it contains barriers).
 template <int NT, uint32_t CMASK, int NC = 1>
 __device__ __forceinline__ void find_digit(const uint32_t *hist, int nb, uint32_t remaining,
                                            uint32_t (*scratch)[NT / 64], int row,
-                                           uint32_t *sel, uint32_t sub0 = 0) {
+                                           uint32_t *sel, int subbin = 0, uint32_t subcnt = 0) {
   const int tid = threadIdx.x;
   const int per = nb / NT;            // nb is a multiple of NT
   const int hi = nb - tid * per;      // thread 0 owns the highest bins
@@ -78,7 +80,7 @@ __device__ __forceinline__ void find_digit(const uint32_t *hist, int nb, uint32_
     uint32_t c = 0;
 #pragma unroll
     for (int x = 0; x < NC; ++x) c += hist[i * NC + x];
-    return i == 0 ? c - sub0 : c;
+    return i == subbin ? c - subcnt : c;
   };
   uint32_t mine = 0;
   for (int i = hi - per; i < hi; ++i) mine += bin(i);
@@ -123,6 +125,18 @@ constexpr int kCopies = 4;
 
 // Two workgroups per CU (16 waves: at most 128 registers a wave), so that a
 // long row and a short one share each CU (see row_of).
+//
+// PACKED (every row starts 16-byte aligned and every candidate count is a
+// multiple of 4): the row is read by 16-byte loads through a buffer resource
+// whose range ends at the row's last candidate, so loads past it return
+// zeros without touching memory and need no per-position test; those npad
+// padding positions are zero keys, taken out of the zero key's bin. The
+// loads hold raw fp32 bits until the first pass forms each run's keys and
+// counts them in load order, so its LDS atomics overlap the loads still in
+// flight (the row load is the largest single cost of a long row).
+// Otherwise each position is tested at load time and padding holds key 0,
+// taken out of bin 0 while every digit fixed so far is 0.
+template <bool PACKED>
 __global__ __launch_bounds__(kRegNT) __attribute__((amdgpu_waves_per_eu(4, 4))) void
 topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ scores,
                 int32_t *__restrict__ idx) {
@@ -151,49 +165,79 @@ topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ sc
   const int nc = L - Wf;
   const int kp = k - Wf;
   const int nsub = (nc + NT * kRun - 1) / (NT * kRun);   // runs in use (<= kRegSub)
-  const bool vec = (((row_id * S) & 3) == 0);            // row start 16-byte aligned
 
-  // Run j of thread t covers positions [kRun*(t + NT*j), +kRun). Positions
-  // at or past nc hold key 0 (kPadKey), which lands in bin 0 of a digit
-  // while every digit fixed so far is 0; those npad keys are taken out of
-  // that bin's count.
-  constexpr uint32_t kPadKey = 0u;
+  // Run j of thread t covers positions [kRun*(t + NT*j), +kRun); npad
+  // positions of the runs in use lie at or past nc.
+  constexpr uint32_t kPadKey = 0u;   // padding key when !PACKED
   const uint32_t npad = (uint32_t)(nsub * NT * kRun - nc);
   uint32_t key[kRegSub][kRun];
+  if constexpr (PACKED) {
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(row), (short)0,
+                                                      (uint32_t)nc * 4u, kTopkBufferDword3);
 #pragma unroll
-  for (int j = 0; j < kRegSub; ++j) {
-    const int p0 = kRun * (tid + NT * j);
+    for (int j = 0; j < kRegSub; ++j) {
+      const uint32_t off = (uint32_t)(kRun * (tid + NT * j)) * 4u;
 #pragma unroll
-    for (int i = 0; i < kRun; i += 4) {
-      float f[4] = {0.f, 0.f, 0.f, 0.f};
-      if (j < nsub) {
-        if (vec && p0 + i + 3 < nc) {
-          const float4 x = *reinterpret_cast<const float4 *>(row + p0 + i);
-          f[0] = x.x; f[1] = x.y; f[2] = x.z; f[3] = x.w;
-        } else {
+      for (int i = 0; i < kRun; i += 4) {
+        // unconditional: a run past nc reads zeros without touching memory,
+        // and the waits of the first pass then count loads exactly
+        const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(rs, off + i * 4, 0, 0);
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (p0 + i + e < nc) f[e] = row[p0 + i + e];
-        }
+        for (int e = 0; e < 4; ++e) key[j][i + e] = x[e];
       }
+    }
+  } else {
+    const bool vec = (((row_id * S) & 3) == 0);   // row start 16-byte aligned
 #pragma unroll
-      for (int e = 0; e < 4; ++e) key[j][i + e] = p0 + i + e < nc ? float_key(f[e]) : kPadKey;
+    for (int j = 0; j < kRegSub; ++j) {
+      const int p0 = kRun * (tid + NT * j);
+#pragma unroll
+      for (int i = 0; i < kRun; i += 4) {
+        float f[4] = {0.f, 0.f, 0.f, 0.f};
+        if (j < nsub) {
+          if (vec && p0 + i + 3 < nc) {
+            const float4 x = *reinterpret_cast<const float4 *>(row + p0 + i);
+            f[0] = x.x; f[1] = x.y; f[2] = x.z; f[3] = x.w;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (p0 + i + e < nc) f[e] = row[p0 + i + e];
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          key[j][i + e] = p0 + i + e < nc ? float_key(f[e]) : kPadKey;
+      }
     }
   }
+  // bin of digit `shift` that the padding keys fall in, if they share `prefix`
+  auto pad_bin = [&](int shift, uint32_t dmask, uint32_t prefix, uint32_t pmask) -> int {
+    const uint32_t pk = PACKED ? kZeroKey : kPadKey;
+    return (pk & pmask) == prefix ? (int)((pk >> shift) & dmask) : -1;
+  };
 
   uint32_t T = 0xffffffffu, remaining = 0;
   if (kp > 0) {
     uint32_t prefix = 0, pmask = 0;
     remaining = (uint32_t)kp;
     uint32_t *discard = hist + kHist + lane;
-#pragma unroll 1
-    for (int pass = 0; pass < 3; ++pass) {
+    // one radix pass; FIRST: the first digit, whose pass also forms the keys
+    // when PACKED
+    auto run_pass = [&](int pass, auto first_) {
+      constexpr bool FORM = PACKED && decltype(first_)::value;
       const int shift = digit_shift(pass), nb = 1 << digit_bits(pass);
       const uint32_t dmask = (uint32_t)nb - 1u;
       const int nco = pass == 0 ? kCopies : 1;   // histogram copies of this digit
       uint32_t *hc = hist + (pass == 0 ? lane % kCopies : 0);
       for (int i = tid; i < nb * nco; i += NT) hist[i] = 0;
-      __syncthreads();
+      if constexpr (FORM) {
+        // LDS-only barrier: the clears are visible, the row loads stay in flight
+        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+        __builtin_amdgcn_s_barrier();
+      } else {
+        __syncthreads();
+      }
       uint32_t zc = 0;
       // opaque to the compiler, so the per-key zero tests stay inside the
       // pass instead of being hoisted out as 64 saved lane masks
@@ -204,7 +248,11 @@ topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ sc
         if (j >= nsub) continue;   // uniform
 #pragma unroll
         for (int i = 0; i < kRun; ++i) {
-          const uint32_t kv = key[j][i];
+          uint32_t kv = key[j][i];
+          if constexpr (FORM) {
+            kv = float_key(__uint_as_float(kv));
+            key[j][i] = kv;
+          }
           const bool in = (kv & pmask) == prefix;
           const bool zero = kv == zkey;
           zc += (in && zero) ? 1u : 0u;
@@ -217,18 +265,24 @@ topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ sc
         if (lane == 0 && zc) atomicAdd(&hist[((kZeroKey >> shift) & dmask) * nco], zc);
       }
       __syncthreads();
-      const uint32_t sub0 = prefix == 0 ? npad : 0u;
+      const int pb = pad_bin(shift, dmask, prefix, pmask);
+      const uint32_t pc = pb >= 0 ? npad : 0u;
       if (pass == 0)
-        find_digit<NT, 0xffffu, kCopies>(hist, nb, remaining, scratch, 0, sel, sub0);
+        find_digit<NT, 0xffffu, kCopies>(hist, nb, remaining, scratch, 0, sel, pb, pc);
       else
-        find_digit<NT, 0xffffu>(hist, nb, remaining, scratch, pass & 1, sel, sub0);
+        find_digit<NT, 0xffffu>(hist, nb, remaining, scratch, pass & 1, sel, pb, pc);
       prefix |= sel[0] << shift;
       pmask |= dmask << shift;
       remaining = sel[1];
       __syncthreads();
-    }
+    };
+    run_pass(0, std::true_type{});
+#pragma unroll 1
+    for (int pass = 1; pass < 3; ++pass) run_pass(pass, std::false_type{});
     T = prefix;
   }
+  // (kp = 0: the emission chooses nothing, whatever the keys hold, so
+  // unformed PACKED keys are harmless there)
 
   // Ordered emission, one run index j at a time (runs of index j, in thread
   // order, cover positions [kRun*NT*j, kRun*NT*(j+1)) in order). Chosen
@@ -413,9 +467,16 @@ hipError_t launch_topk(const Prob &p, const float *scores, int32_t *idx, hipStre
   // Longest candidate range of any row: the last block's causal length minus the window.
   const int Lmax = min(p.qo + p.R * p.b, p.S);
   const int ncmax = Lmax - min(p.W, p.k);
-  if (ncmax <= kRegCap)
-    hipLaunchKernelGGL(topk_reg_kernel, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kRegNT), 0, st, p.S,
-                       p.qo, p.b, p.k, p.W, scores, idx);
+  // every row 16-byte aligned and every candidate count (L - min(W, k), with
+  // L = min(qo + (r + 1) b, S)) a multiple of 4
+  const bool packed = ((uintptr_t)scores & 15) == 0 && p.S % 4 == 0 && p.qo % 4 == 0 &&
+                      p.b % 4 == 0 && min(p.W, p.k) % 4 == 0;
+  if (ncmax <= kRegCap && packed)
+    hipLaunchKernelGGL(topk_reg_kernel<true>, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kRegNT), 0, st,
+                       p.S, p.qo, p.b, p.k, p.W, scores, idx);
+  else if (ncmax <= kRegCap)
+    hipLaunchKernelGGL(topk_reg_kernel<false>, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kRegNT), 0, st,
+                       p.S, p.qo, p.b, p.k, p.W, scores, idx);
   else
     hipLaunchKernelGGL(topk_rows_kernel, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kNT), 0, st, p.S,
                        p.qo, p.b, p.k, p.W, scores, idx);
