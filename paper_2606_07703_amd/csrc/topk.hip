@@ -126,16 +126,17 @@ constexpr int kCopies = 4;
 // Two workgroups per CU (16 waves: at most 128 registers a wave), so that a
 // long row and a short one share each CU (see row_of).
 //
-// PACKED (every row starts 16-byte aligned and every candidate count is a
-// multiple of 4): the row is read by 16-byte loads through a buffer resource
-// whose range ends at the row's last candidate, so loads past it return
-// zeros without touching memory and need no per-position test; those npad
-// padding positions are zero keys, taken out of the zero key's bin. The
-// loads hold raw fp32 bits until the first pass forms each run's keys and
-// counts them in load order, so its LDS atomics overlap the loads still in
-// flight (the row load is the largest single cost of a long row).
-// Otherwise each position is tested at load time and padding holds key 0,
-// taken out of bin 0 while every digit fixed so far is 0.
+// PACKED (every row starts 16-byte aligned): the row is read by 16-byte
+// loads through a buffer resource whose range ends at the row's last
+// candidate. Raw buffer loads check that range per dword: the dwords past it
+// read as zeros without touching memory, also inside a load that straddles
+// it, so no position is tested and no load is guarded; those npad padding
+// positions are zero keys, taken out of the zero key's bin. The loads hold
+// raw fp32 bits until the first pass forms each run's keys and counts them
+// in load order, so its LDS atomics overlap the loads still in flight (the
+// row load is the largest single cost of a long row). Otherwise each
+// position is tested at load time and padding holds key 0, taken out of
+// bin 0 while every digit fixed so far is 0.
 template <bool PACKED>
 __global__ __launch_bounds__(kRegNT) __attribute__((amdgpu_waves_per_eu(4, 4))) void
 topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ scores,
@@ -467,10 +468,8 @@ hipError_t launch_topk(const Prob &p, const float *scores, int32_t *idx, hipStre
   // Longest candidate range of any row: the last block's causal length minus the window.
   const int Lmax = min(p.qo + p.R * p.b, p.S);
   const int ncmax = Lmax - min(p.W, p.k);
-  // every row 16-byte aligned and every candidate count (L - min(W, k), with
-  // L = min(qo + (r + 1) b, S)) a multiple of 4
-  const bool packed = ((uintptr_t)scores & 15) == 0 && p.S % 4 == 0 && p.qo % 4 == 0 &&
-                      p.b % 4 == 0 && min(p.W, p.k) % 4 == 0;
+  // every row starts 16-byte aligned
+  const bool packed = ((uintptr_t)scores & 15) == 0 && p.S % 4 == 0;
   if (ncmax <= kRegCap && packed)
     hipLaunchKernelGGL(topk_reg_kernel<true>, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kRegNT), 0, st,
                        p.S, p.qo, p.b, p.k, p.W, scores, idx);

@@ -219,6 +219,8 @@ TOPK_CASES = [
     (30000, 64, 512, 16, "coarse"),    # long rows of 16 levels: crowded bins
     (3000, 12, 300, 8, "relu"),        # 16-byte row loads, candidate counts 4 mod 16
     (4000, 4, 256, 4, "coarse"),       # 16-byte row loads, 4-query blocks
+    (4999, 1, 64, 3, "relu"),          # rows not 16-byte aligned: tested loads
+    (3001, 64, 500, 0, "gauss"),       # rows not 16-byte aligned, 64-query blocks
     (70000, 70000, 40000, 0, "const"), # streamed row: one thread's bins hold > 65535 keys
     (70000, 35000, 3000, 17, "relu"),  # streamed rows with ReLU zeros and a window
 ]
