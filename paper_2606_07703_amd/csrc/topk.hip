@@ -219,6 +219,7 @@ topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ sc
   };
 
   uint32_t T = 0xffffffffu, remaining = 0;
+  uint32_t ties = 0;   // candidates whose key equals T
   if (kp > 0) {
     uint32_t prefix = 0, pmask = 0;
     remaining = (uint32_t)kp;
@@ -272,6 +273,8 @@ topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ sc
         find_digit<NT, 0xffffu, kCopies>(hist, nb, remaining, scratch, 0, sel, pb, pc);
       else
         find_digit<NT, 0xffffu>(hist, nb, remaining, scratch, pass & 1, sel, pb, pc);
+      // after the last digit, the chosen bin holds exactly the keys equal to T
+      if (pass == 2) ties = hist[sel[0]] - (pb == (int)sel[0] ? npad : 0u);
       prefix |= sel[0] << shift;
       pmask |= dmask << shift;
       remaining = sel[1];
@@ -282,13 +285,43 @@ topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ sc
     for (int pass = 1; pass < 3; ++pass) run_pass(pass, std::false_type{});
     T = prefix;
   }
-  // (kp = 0: the emission chooses nothing, whatever the keys hold, so
-  // unformed PACKED keys are harmless there)
+  // (kp = 0: nothing is chosen; unformed PACKED keys are never read)
 
   // Ordered emission, one run index j at a time (runs of index j, in thread
   // order, cover positions [kRun*NT*j, kRun*NT*(j+1)) in order). Chosen
   // positions are written to their output slot in LDS (hist, free after the
   // passes) when the row fits, then copied out with coalesced stores.
+  //
+  // When every key equal to T is taken (the usual case: T is one key), the
+  // chosen set is {key >= T}: one mask and one count per run.
+  auto emit_all = [&](auto staged_tag) {
+    constexpr bool STAGED = decltype(staged_tag)::value;
+    uint32_t before = 0;
+#pragma unroll
+    for (int j = 0; j < kRegSub; ++j) {
+      if (j >= nsub) break;   // uniform
+      const int p0 = kRun * (tid + NT * j);
+      const int nv = min(max(nc - p0, 0), kRun);   // this run's real positions
+      uint32_t take = 0;
+#pragma unroll
+      for (int i = 0; i < kRun; ++i) take |= key[j][i] >= T ? 1u << i : 0u;
+      take &= (1u << nv) - 1u;   // nv <= 16
+      uint32_t total;
+      const uint32_t ex =
+          scan_bits<NT, 0x1fu>((uint32_t)__popc(take), scratch, (j + 1) & 1, &total);
+      uint32_t pos = before + ex;
+      while (take) {
+        const int i = __builtin_ctz(take);
+        take &= take - 1u;
+        if constexpr (STAGED)
+          hist[pos] = (uint32_t)(p0 + i);
+        else if (pos < (uint32_t)kp)   // always true for consistent counts
+          out[pos] = p0 + i;
+        ++pos;
+      }
+      before += total;
+    }
+  };
   auto emit = [&](auto staged_tag) {
     constexpr bool STAGED = decltype(staged_tag)::value;
     uint32_t gt_before = 0, eq_before = 0;
@@ -340,12 +373,20 @@ topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ sc
       eq_before += total & 0xffffu;
     }
   };
-  if (kp <= kHist) {
-    emit(std::true_type{});
-    __syncthreads();
-    for (int c = tid; c < kp; c += NT) out[c] = (int32_t)hist[c];
-  } else {
-    emit(std::false_type{});
+  if (kp > 0) {
+    const bool all = ties == remaining;   // uniform
+    if (kp <= kHist) {
+      if (all)
+        emit_all(std::true_type{});
+      else
+        emit(std::true_type{});
+      __syncthreads();
+      for (int c = tid; c < kp; c += NT) out[c] = (int32_t)hist[c];
+    } else if (all) {
+      emit_all(std::false_type{});
+    } else {
+      emit(std::false_type{});
+    }
   }
   for (int c = tid; c < Wf; c += NT) out[kp + c] = nc + c;
 }
