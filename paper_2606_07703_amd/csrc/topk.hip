@@ -122,6 +122,9 @@ constexpr int kRegCap = kRegNT * kRun * kRegSub;   // 32768 candidates
 // one wave's atomics on them; the later digits, over keys sharing the first,
 // spread out and use one copy.
 constexpr int kCopies = 4;
+// Keys sharing the 22-bit prefix of T gathered for a direct search (at most
+// one per thread) instead of the third histogram pass.
+constexpr int kCand = 256;
 
 // Two workgroups per CU (16 waves: at most 128 registers a wave), so that a
 // long row and a short one share each CU (see row_of).
@@ -148,7 +151,7 @@ topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ sc
   // atomic and no branch); after the passes, the output row is staged here
   __shared__ uint32_t hist[kHist + 64];
   __shared__ uint32_t scratch[2][NT / 64];
-  __shared__ uint32_t sel[2];
+  __shared__ uint32_t sel[3];
 
   const int r = row_of((int)blockIdx.x, (int)gridDim.x);
   const int tid = threadIdx.x, lane = tid & 63;
@@ -273,17 +276,60 @@ topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ sc
         find_digit<NT, 0xffffu, kCopies>(hist, nb, remaining, scratch, 0, sel, pb, pc);
       else
         find_digit<NT, 0xffffu>(hist, nb, remaining, scratch, pass & 1, sel, pb, pc);
-      // after the last digit, the chosen bin holds exactly the keys equal to T
-      if (pass == 2) ties = hist[sel[0]] - (pb == (int)sel[0] ? npad : 0u);
+      // the chosen bin's keys: after the second digit, the candidates of the
+      // third; after the last digit, exactly the keys equal to T
+      if (pass >= 1) ties = hist[sel[0]] - (pb == (int)sel[0] ? npad : 0u);
       prefix |= sel[0] << shift;
       pmask |= dmask << shift;
       remaining = sel[1];
       __syncthreads();
     };
     run_pass(0, std::true_type{});
-#pragma unroll 1
-    for (int pass = 1; pass < 3; ++pass) run_pass(pass, std::false_type{});
-    T = prefix;
+    run_pass(1, std::false_type{});
+    // Third digit. When few keys share the 22-bit prefix (and no zero or
+    // padding key does), they are gathered into LDS and T is found among
+    // them directly: each gathered key counts the gathered keys above it
+    // and equal to it. Otherwise a third histogram pass.
+    const uint32_t pad_key = PACKED ? kZeroKey : kPadKey;
+    if (ties <= kCand && (kZeroKey & pmask) != prefix && (pad_key & pmask) != prefix) {
+      const uint32_t n1 = ties;
+      uint32_t *cnt = hist + kHist;   // a discard word, free after the passes
+      if (tid == 0) *cnt = 0u;
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < kRegSub; ++j) {
+        if (j >= nsub) continue;   // uniform
+#pragma unroll
+        for (int i = 0; i < kRun; ++i) {
+          const uint32_t kv = key[j][i];
+          if ((kv & pmask) == prefix) hist[atomicAdd(cnt, 1u)] = kv;
+        }
+      }
+      __syncthreads();
+      if (tid < (int)n1) {
+        const uint32_t v = hist[tid];
+        uint32_t above = 0, same = 0;
+        for (uint32_t c = 0; c < n1; ++c) {
+          const uint32_t u = hist[c];
+          above += u > v ? 1u : 0u;
+          same += u == v ? 1u : 0u;
+        }
+        // v is T: the remaining-th largest of the gathered keys (equal keys
+        // write the same values)
+        if (above < remaining && remaining <= above + same) {
+          sel[0] = v;
+          sel[1] = remaining - above;
+          sel[2] = same;
+        }
+      }
+      __syncthreads();
+      T = sel[0];
+      remaining = sel[1];
+      ties = sel[2];
+    } else {
+      run_pass(2, std::false_type{});
+      T = prefix;
+    }
   }
   // (kp = 0: nothing is chosen; unformed PACKED keys are never read)
 

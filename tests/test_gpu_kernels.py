@@ -262,6 +262,33 @@ def test_topk_streamed_crowded_bins():
     assert np.array_equal(idx.cpu().numpy(), ref)
 
 
+@pytest.mark.parametrize("n_close", [200, 256, 257, 300])
+def test_topk_keys_sharing_the_high_bits(n_close):
+    """Rows whose k-th largest key shares its top 22 bits with n_close keys
+    (values 1 + m 2^-23, m < 64: many exact ties): up to 256 such keys the
+    threshold is searched among them directly, beyond that by a third radix
+    pass. Both must match the oracle bit for bit."""
+    S, k = 4096, 150
+    say(f"topk keys sharing the high bits {n_close}")
+    rng = np.random.default_rng(100 + n_close)
+    rows = []
+    for _ in range(3):
+        row = rng.uniform(-1.0, 0.5, S).astype(np.float32)
+        pos = rng.choice(S, n_close, replace=False)
+        m = rng.integers(0, 64, n_close)
+        row[pos] = (np.float32(1.0) + m.astype(np.float32) * np.float32(2.0 ** -23))
+        rows.append(row)
+    scores = torch.from_numpy(np.stack(rows))
+    p = B.Problem(S, 1, 1, 64, topk=k, block_q=S, dtype="f32")
+    # three rows of one block each: lay them out as a batch of three problems
+    for r in range(3):
+        idx = torch.empty(1, k, dtype=torch.int32, device="cuda")
+        B.sp_topk_select(p, cuda(scores[r:r + 1].contiguous()), idx)
+        torch.cuda.synchronize()
+        ref = oracle.topk(scores[r:r + 1].numpy().astype(np.float64), np.array([S]), k, 0)
+        assert np.array_equal(idx.cpu().numpy(), ref)
+
+
 # --------------------------------------------------------------- indexer scores
 INDEXER_CASES = [
     # S, d_idx, b, agg, relu, dtype
