@@ -568,28 +568,59 @@ struct AttnPipe {
 };
 
 // Final normalisation: writes o (bf16, if non-null) and lse (natural log, if
-// non-null) for this lane's row if it is valid. Rows with no usable key get
-// o = 0 and lse = -inf.
+// non-null) for this wave's valid rows. Rows with no usable key get o = 0 and
+// lse = -inf.
+//
+// O is held transposed (lane (n, h) has 8-byte pieces of row n), and stored
+// from there each instruction would scatter 16 bytes over 32 rows. Instead
+// every wave writes its 32 normalised rows into a private slice of the tile
+// buffers (idle once every wave has left the pipeline), reads them back
+// row-major and stores whole rows: 1 KiB of consecutive rows per
+// instruction. A row's destination comes from the lane that owns it by a
+// lane shuffle. Every wave of the workgroup calls this (it starts with a
+// workgroup barrier); lds is the pipeline's tile storage.
 template <int D>
 __device__ __forceinline__ void attn_finish(const AttnState<D> &st, const QRow<D> &qr, int Hq,
                                             uint16_t *__restrict__ o, float *__restrict__ lse,
-                                            int h) {
+                                            int h, char *lds) {
+  using L = AttnLayout<D>;
   const float l = half_sum(st.l);
-  if (!qr.valid) return;
-  const size_t row = (size_t)qr.t * Hq + qr.head;
-  if (lse && h == 0) lse[row] = l > 0.f ? (st.m + log2f(l)) * kLn2 : -INFINITY;
-  if (o) {
-    const float inv = l > 0.f ? 1.f / l : 0.f;
-    uint16_t *op = o + row * D + 4 * h;
+  if (lse && h == 0 && qr.valid)
+    lse[(size_t)qr.t * Hq + qr.head] = l > 0.f ? (st.m + log2f(l)) * kLn2 : -INFINITY;
+  if (!o) return;
+  // slice row stride: 16 rows of a 64-lane write land on distinct bank pairs
+  constexpr int OS = L::RB + 16;
+  static_assert(kAttnQPW * OS * attn_max_waves<D>() <= L::bytes(true), "slices fit the tiles");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  char *slice = lds + wave * kAttnQPW * OS;
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  __syncthreads();
+  char *wr = slice + (lane & 31) * OS + 8 * h;
 #pragma unroll
-    for (int dt = 0; dt < AttnLayout<D>::DT; ++dt)
+  for (int dt = 0; dt < L::DT; ++dt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        uint2 w;
-        w.x = pack_bf16x2(st.o[dt][4 * i] * inv, st.o[dt][4 * i + 1] * inv);
-        w.y = pack_bf16x2(st.o[dt][4 * i + 2] * inv, st.o[dt][4 * i + 3] * inv);
-        *reinterpret_cast<uint2 *>(op + 32 * dt + 8 * i) = w;
-      }
+    for (int i = 0; i < 4; ++i) {
+      uint2 w;
+      w.x = pack_bf16x2(st.o[dt][4 * i] * inv, st.o[dt][4 * i + 1] * inv);
+      w.y = pack_bf16x2(st.o[dt][4 * i + 2] * inv, st.o[dt][4 * i + 3] * inv);
+      *reinterpret_cast<uint2 *>(wr + 64 * dt + 16 * i) = w;
+    }
+  // the reads below take other lanes' rows
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  constexpr int LPR = L::RB / 16;   // lanes per row
+  constexpr int RPI = 64 / LPR;     // rows per store instruction
+  const int rr = lane / LPR, cc = lane % LPR;
+  const int my_t = qr.valid ? qr.t : -1;
+#pragma unroll
+  for (int it = 0; it < kAttnQPW / RPI; ++it) {
+    const int m = it * RPI + rr;
+    const int t = __shfl(my_t, m, 64);
+    const int head = __shfl(qr.head, m, 64);
+    const int4 val = *reinterpret_cast<const int4 *>(slice + m * OS + cc * 16);
+    if (t >= 0)
+      *reinterpret_cast<int4 *>(o + ((size_t)t * Hq + head) * D + cc * 8) = val;
   }
 }
 

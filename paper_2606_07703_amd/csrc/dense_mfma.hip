@@ -59,7 +59,7 @@ __global__ __launch_bounds__(attn_max_waves<D>() * 64) SP_ATTN_OCCUPANCY(D) void
   AttnPipe<D, kNW, WANT_O, DenseKeys> pipe(lds, keys, k, v, S, Hkv, j, scale_log2, wave_tmin, qr,
                                            st);
   pipe.run();
-  attn_finish<D>(st, qr, Hq, WANT_O ? o : nullptr, lse, h);
+  attn_finish<D>(st, qr, Hq, WANT_O ? o : nullptr, lse, h, lds);
 }
 
 template <int D>

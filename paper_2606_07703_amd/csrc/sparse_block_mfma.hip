@@ -162,7 +162,7 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY(D) void sparse_block_ker
   AttnPipe<D, NW, true, SupportKeys> pipe(lds, keys, k, v, kv_rows, Hkv, j, scale_log2, wave_tmin,
                                           qr, st);
   pipe.run();
-  attn_finish<D>(st, qr, Hq, o, nullptr, h);
+  attn_finish<D>(st, qr, Hq, o, nullptr, h, lds);
 }
 
 template <int D, bool PAGED>
