@@ -14,7 +14,7 @@
 //
 // Workgroups are numbered with the KV head fastest: consecutive workgroups go
 // to different XCDs, so with Hkv = 8 each XCD's L2 holds the K/V rows of one
-// head only.
+// head only. Blocks are dispatched from the last to the first.
 #include <limits.h>
 
 #include "attn_tile.hpp"
@@ -74,7 +74,11 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY(D) void sparse_block_ker
   const int j = (int)blockIdx.x % Hkv;
   const int rest = (int)blockIdx.x / Hkv;
   const int chunk = rest % nchunks;
-  const int r = rest / nchunks;   // counts blocks from the chunk start
+  // blocks run last to first: the supports of the first blocks are cut short
+  // by the causal limit, and those small workgroups then fill the end of the
+  // launch instead of its start
+  const int nblocks = (int)gridDim.x / (Hkv * nchunks);
+  const int r = nblocks - 1 - rest / nchunks;   // counts blocks from the chunk start
   const int t0 = qo + r * b;
   const int t1 = min(t0 + b, S) - 1;
   const int nrows = (t1 - t0 + 1) * G;
