@@ -443,6 +443,10 @@ constexpr int kEmitPer = 16;
 constexpr int kEmitChunk = kNT * kEmitPer;
 constexpr int kEmitStride = kNT + 4;   // LDS column stride: conflict-free writes and reads
 
+// VEC: every row starts 16-byte aligned and S % 4 == 0, so the histogram
+// passes read four keys per load, sixteen per thread in flight; otherwise
+// one key per load.
+template <bool VEC>
 __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, int k, int W,
                                                         const float *__restrict__ scores,
                                                         int32_t *__restrict__ idx) {
@@ -480,12 +484,35 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, in
       for (int i = tid; i < nb; i += kNT) hist[i] = 0;
       __syncthreads();
       uint32_t zc = 0;
-      for (int i = tid; i < nc; i += kNT) {
-        const uint32_t kv = float_key(row[i]);
+      auto count = [&](uint32_t kv) {
         if ((kv & pmask) == prefix) {
           if (kv == kZeroKey) ++zc;
           else atomicAdd(&hist[(kv >> shift) & dmask], 1u);
         }
+      };
+      if constexpr (VEC) {
+        // a step covers 16 NT positions: thread tid reads positions
+        // 4(tid + NT u) .. +3 for u < 4; a load that starts below nc ends
+        // below S (nc <= S, both steps of 4), inside the row
+        for (int base = 0; base < nc; base += 16 * kNT) {
+          float4 x[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int p0 = base + 4 * (tid + kNT * u);
+            x[u] = p0 < nc ? *reinterpret_cast<const float4 *>(row + p0)
+                           : float4{0.f, 0.f, 0.f, 0.f};
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int p0 = base + 4 * (tid + kNT * u);
+            const float v4[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (p0 + e < nc) count(float_key(v4[e]));
+          }
+        }
+      } else {
+        for (int i = tid; i < nc; i += kNT) count(float_key(row[i]));
       }
       if ((kZeroKey & pmask) == prefix) {
 #pragma unroll
@@ -563,9 +590,12 @@ hipError_t launch_topk(const Prob &p, const float *scores, int32_t *idx, hipStre
   else if (ncmax <= kRegCap)
     hipLaunchKernelGGL(topk_reg_kernel<false>, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kRegNT), 0, st,
                        p.S, p.qo, p.b, p.k, p.W, scores, idx);
+  else if (packed)
+    hipLaunchKernelGGL(topk_rows_kernel<true>, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kNT), 0, st,
+                       p.S, p.qo, p.b, p.k, p.W, scores, idx);
   else
-    hipLaunchKernelGGL(topk_rows_kernel, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kNT), 0, st, p.S,
-                       p.qo, p.b, p.k, p.W, scores, idx);
+    hipLaunchKernelGGL(topk_rows_kernel<false>, dim3(p.R, p.ha ? p.Hkv : 1), dim3(kNT), 0, st,
+                       p.S, p.qo, p.b, p.k, p.W, scores, idx);
   return hipGetLastError();
 }
 

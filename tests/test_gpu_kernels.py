@@ -223,6 +223,8 @@ TOPK_CASES = [
     (3001, 64, 500, 0, "gauss"),       # rows not 16-byte aligned, 64-query blocks
     (70000, 70000, 40000, 0, "const"), # streamed row: one thread's bins hold > 65535 keys
     (70000, 35000, 3000, 17, "relu"),  # streamed rows with ReLU zeros and a window
+    (69996, 34998, 2048, 1, "coarse"), # streamed 16-byte loads, candidate counts 1 and 3 mod 4
+    (70001, 35001, 3000, 5, "gauss"),  # streamed rows not 16-byte aligned: one key per load
 ]
 
 
