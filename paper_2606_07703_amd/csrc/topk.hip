@@ -438,14 +438,15 @@ topk_reg_kernel(int S, int qo, int b, int k, int W, const float *__restrict__ sc
 }
 
 // -------------------------------------------------------------- streamed rows
-constexpr int kNT = 256;
+constexpr int kNT = 512;
 constexpr int kEmitPer = 16;
 constexpr int kEmitChunk = kNT * kEmitPer;
 constexpr int kEmitStride = kNT + 4;   // LDS column stride: conflict-free writes and reads
 
-// VEC: every row starts 16-byte aligned and S % 4 == 0, so the histogram
-// passes read four keys per load, sixteen per thread in flight; otherwise
-// one key per load.
+// VEC: every row starts 16-byte aligned and S % 4 == 0, so the passes read
+// four keys per load through range-checked buffer loads, the next step's in
+// flight while a step is counted; otherwise one key per load, and the
+// emission stages its keys in LDS.
 template <bool VEC>
 __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, int k, int W,
                                                         const float *__restrict__ scores,
@@ -453,7 +454,6 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, in
   __shared__ uint32_t hist[2048];
   __shared__ uint32_t scratch[2][kNT / 64];
   __shared__ uint32_t sel[2];
-  __shared__ uint32_t keys[kEmitPer * kEmitStride];
 
   const int r = row_of((int)blockIdx.x, (int)gridDim.x);
   const int tid = threadIdx.x, lane = tid & 63;
@@ -491,25 +491,37 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, in
         }
       };
       if constexpr (VEC) {
-        // a step covers 16 NT positions: thread tid reads positions
-        // 4(tid + NT u) .. +3 for u < 4; a load that starts below nc ends
-        // below S (nc <= S, both steps of 4), inside the row
-        for (int base = 0; base < nc; base += 16 * kNT) {
-          float4 x[4];
+        // A step covers 16 NT positions: thread tid reads positions
+        // 4(tid + NT u) .. +3 for u < 4, through a buffer resource ranged to
+        // the nc candidates (reads past them return zeros, which are not
+        // counted). The loads are unconditional, so the next step's are in
+        // flight while this step is counted.
+        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+        const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(row), (short)0,
+                                                          (uint32_t)nc * 4u, kTopkBufferDword3);
+        constexpr int kStep = 16 * kNT;
+        auto load = [&](u32x4 (&x)[4], int base) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            x[u] = __builtin_amdgcn_raw_buffer_load_b128(
+                rs, (uint32_t)(base + 4 * (tid + kNT * u)) * 4u, 0, 0);
+        };
+        auto counts = [&](const u32x4 (&x)[4], int base) {
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
             const int p0 = base + 4 * (tid + kNT * u);
-            x[u] = p0 < nc ? *reinterpret_cast<const float4 *>(row + p0)
-                           : float4{0.f, 0.f, 0.f, 0.f};
-          }
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int p0 = base + 4 * (tid + kNT * u);
-            const float v4[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-              if (p0 + e < nc) count(float_key(v4[e]));
+              if (p0 + e < nc) count(float_key(__uint_as_float(x[u][e])));
           }
+        };
+        u32x4 xa[4], xb[4];
+        load(xa, 0);
+        for (int base = 0; base < nc; base += 2 * kStep) {
+          load(xb, base + kStep);
+          counts(xa, base);
+          load(xa, base + 2 * kStep);
+          counts(xb, base + kStep);
         }
       } else {
         for (int i = tid; i < nc; i += kNT) count(float_key(row[i]));
@@ -530,48 +542,84 @@ __global__ __launch_bounds__(kNT) void topk_rows_kernel(int S, int qo, int b, in
     T = prefix;
   }
 
-  // Ordered emission over candidates in chunks of kEmitChunk positions; in
-  // LDS, position q of a chunk sits at (q % kEmitPer) * kEmitStride + q / kEmitPer.
+  // Ordered emission over candidates in chunks of kEmitChunk positions;
+  // thread tid takes the kEmitPer consecutive positions from kEmitPer * tid.
   uint32_t gt_before = 0, eq_before = 0;
   int srow = 1;
-  for (int base = 0; base < nc; base += kEmitChunk, srow ^= 1) {
-    const int n = min(kEmitChunk, nc - base);
-    for (int i = tid; i < kEmitChunk; i += kNT)
-      keys[(i % kEmitPer) * kEmitStride + i / kEmitPer] = i < n ? float_key(row[base + i]) : 0u;
-    __syncthreads();
-    const int lo = tid * kEmitPer;
+  // Counts a chunk's keys above and on the threshold, scans them over the
+  // block and writes the chosen positions (key(e) is the key at lo + e).
+  auto emit_chunk = [&](int base, auto key) {
+    const int lo = base + tid * kEmitPer;
     uint32_t cgt = 0, ceq = 0;
 #pragma unroll
     for (int e = 0; e < kEmitPer; ++e) {
-      if (lo + e < n) {
-        const uint32_t kv = keys[e * kEmitStride + tid];
+      if (lo + e < nc) {
+        const uint32_t kv = key(e);
         cgt += kv > T;
         ceq += kv == T;
       }
     }
     uint32_t total;
     const uint32_t ex = scan_bits<kNT, 0x1f001fu>((cgt << 16) | ceq, scratch, srow, &total);
+    srow ^= 1;
     uint32_t my_gt = gt_before + (ex >> 16);
     uint32_t my_eq = eq_before + (ex & 0xffffu);
     uint32_t pos = my_gt + min(my_eq, remaining);
 #pragma unroll
     for (int e = 0; e < kEmitPer; ++e) {
-      if (lo + e < n) {
-        const uint32_t kv = keys[e * kEmitStride + tid];
+      if (lo + e < nc) {
+        const uint32_t kv = key(e);
         bool take = kv > T;
         if (kv == T) {
           take = my_eq < remaining;
           ++my_eq;
         }
         if (take) {
-          if (pos < (uint32_t)kp) out[pos] = base + lo + e;   // always true for consistent counts
+          if (pos < (uint32_t)kp) out[pos] = lo + e;   // always true for consistent counts
           ++pos;
         }
       }
     }
     gt_before += total >> 16;
     eq_before += total & 0xffffu;
-    __syncthreads();
+  };
+  if constexpr (VEC) {
+    // Each thread's 16 positions are four 16-byte loads through a buffer
+    // resource ranged to the candidates (zeros past nc, not counted); the
+    // next chunk's loads are in flight while a chunk is counted and emitted.
+    // No LDS staging: scan_bits alternates its two scratch rows, so one
+    // barrier per chunk (inside the scan) suffices.
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(row), (short)0,
+                                                      (uint32_t)nc * 4u, kTopkBufferDword3);
+    auto load = [&](u32x4 (&x)[4], int base) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        x[u] = __builtin_amdgcn_raw_buffer_load_b128(
+            rs, (uint32_t)(base + tid * kEmitPer + 4 * u) * 4u, 0, 0);
+    };
+    u32x4 xa[4], xb[4];
+    load(xa, 0);
+    for (int base = 0; base < nc; base += 2 * kEmitChunk) {
+      load(xb, base + kEmitChunk);
+      emit_chunk(base, [&](int e) { return float_key(__uint_as_float(xa[e >> 2][e & 3])); });
+      load(xa, base + 2 * kEmitChunk);
+      if (base + kEmitChunk < nc)
+        emit_chunk(base + kEmitChunk,
+                   [&](int e) { return float_key(__uint_as_float(xb[e >> 2][e & 3])); });
+    }
+  } else {
+    // Keys pass through LDS: position q of a chunk sits at
+    // (q % kEmitPer) * kEmitStride + q / kEmitPer.
+    __shared__ uint32_t keys[kEmitPer * kEmitStride];
+    for (int base = 0; base < nc; base += kEmitChunk) {
+      const int n = min(kEmitChunk, nc - base);
+      for (int i = tid; i < kEmitChunk; i += kNT)
+        keys[(i % kEmitPer) * kEmitStride + i / kEmitPer] = i < n ? float_key(row[base + i]) : 0u;
+      __syncthreads();
+      emit_chunk(base, [&](int e) { return keys[e * kEmitStride + tid]; });
+      __syncthreads();
+    }
   }
   for (int c = tid; c < Wf; c += kNT) out[kp + c] = nc + c;
 }
