@@ -70,25 +70,36 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 
 template <int D>
 struct AttnLayout {
-  // K and V tiles (64 rows of D bf16) are row-major with padded rows. K row
+  // K and V tiles (64 rows of D bf16) are row-major. K rows are padded: row
   // stride KRB puts the 16 rows of a b128 operand-read phase on distinct
-  // banks; V row stride VRB puts the 4 rows of a transpose-read phase 16
-  // banks apart. Every operand read is then one lane base plus an immediate
+  // banks. V rows are not padded; instead the 64-byte groups of row r are
+  // permuted, group g stored at g ^ vswz(r), so the 4 rows a transpose-read
+  // phase touches land on 4 different 16-bank groups. The permutation
+  // depends only on r mod 4 (r mod 4 / 2 at D = 64), so every K read, and
+  // every V read of one 32-dim block, is one lane base plus an immediate
   // offset. A tile is a whole number of 1 KiB chunks (the unit of a
   // direct-to-LDS load).
   static constexpr int RB = D * 2;            // bytes of one row in HBM
   static constexpr int C = D / 8;             // 16-byte columns of a row
   static constexpr int KSLOTS = C + 1;        // 16-byte slots of a K row
-  static constexpr int VSLOTS = C + 4;        // 16-byte slots of a V row
+  static constexpr int VSLOTS = C;            // 16-byte slots of a V row
   static constexpr int KRB = 16 * KSLOTS;
   static constexpr int VRB = 16 * VSLOTS;
   static constexpr int KTILE = kAttnKT * KRB;
   static constexpr int VTILE = kAttnKT * VRB;
   static_assert(KTILE % 1024 == 0 && VTILE % 1024 == 0, "tiles are whole chunks");
   static constexpr int KS = D / 16;   // k-steps of K Q^T
-  static constexpr int DT = D / 32;   // 32-row blocks of O^T
+  static constexpr int DT = D / 32;   // 32-row blocks of O^T (64-byte groups of a V row)
+  __host__ __device__ static constexpr int vswz(int r) { return DT >= 4 ? (r & 3) : ((r >> 1) & 1); }
   // two K buffers, then (when the output is wanted) two V buffers
   static constexpr int bytes(bool want_v) { return 2 * KTILE + (want_v ? 2 * VTILE : 0); }
+  // the output staging of attn_finish reuses the tiles: 32 rows per wave at
+  // a stride of RB + 16 bytes
+  static constexpr int FINISH_OS = RB + 16;
+  static constexpr int lds_bytes(bool want_v, int nw) {
+    return want_v && nw * kAttnQPW * FINISH_OS > bytes(true) ? nw * kAttnQPW * FINISH_OS
+                                                             : bytes(want_v);
+  }
 };
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -132,9 +143,10 @@ __device__ __forceinline__ int4 lds_read_i32x4(uint32_t a) {
 // Global -> LDS staging of one tile of K or V rows of KV head j, with no
 // register round trip: a load instruction fills one 1 KiB chunk of the tile
 // (buffer_load_dwordx4 ... lds puts lane L's 16 bytes at byte 16L of it).
-// Lane L of chunk q holds 16-byte slot 64q + L of the padded tile, that is
-// row (64q + L) / SLOTS, column (64q + L) % SLOTS; lanes on padding slots
-// load nothing. The chunks of a tile go to the waves in turn.
+// Lane L of chunk q holds 16-byte slot 64q + L of the tile, that is row
+// (64q + L) / SLOTS, stored column (64q + L) % SLOTS. K: lanes on padding
+// slots load nothing. V: the lane fetches the column whose permuted place
+// that slot is. The chunks of a tile go to the waves in turn.
 template <int D, int NW, bool IS_V>
 struct TileLoader {
   using L = AttnLayout<D>;
@@ -172,7 +184,8 @@ struct TileLoader {
     for (int p = 0; p < PER; ++p) {
       const int q = wave + p * NW;
       const int slot = (q < CHUNKS ? q : 0) * 64 + lane;
-      const int c = slot % SLOTS;
+      int c = slot % SLOTS;
+      if constexpr (IS_V) c ^= 4 * L::vswz(slot / SLOTS);
       const uint32_t s = (rw[p] >= 0 && rw[p] < nrows) ? (uint32_t)rw[p] : 0u;
       const uint32_t off = s * row_bytes + (uint32_t)(j * L::RB + (c < L::C ? c : 0) * 16);
       if (CHUNKS % NW == 0 || q < CHUNKS)
@@ -235,16 +248,20 @@ struct AttnState {
 // This lane's read offsets into a K tile and a V tile. K fragment (kb, ks)
 // of lane (n, h) is row 32kb + n, bytes 32ks + 16h. V^T fragment (f, dt) of
 // lane (grp, c16) reads, by transpose, rows 16f + 4h + c16/4 (then +8),
-// d = 32dt + 16(grp%2) + 4(c16%4) onwards. The parts that depend on kb, ks,
-// f and dt are immediate offsets.
+// d = 32dt + 16(grp%2) + 4(c16%4) onwards, whose 64-byte group dt is stored
+// at dt ^ vswz(row): one base per d-block dt (the same for all the rows this
+// lane reads). The parts that depend on kb, ks and f are immediate offsets.
 template <int D>
 struct TileOffsets {
   using L = AttnLayout<D>;
-  uint32_t k, v;
+  uint32_t k, v[L::DT];
   __device__ __forceinline__ void init(int lane) {
     const int n = lane & 31, h = lane >> 5, c16 = lane & 15, grp = lane >> 4;
     k = n * L::KRB + h * 16;
-    v = (4 * h + (c16 >> 2)) * L::VRB + 32 * (grp & 1) + 8 * (c16 & 3);
+    const int r0 = 4 * h + (c16 >> 2);
+#pragma unroll
+    for (int dt = 0; dt < L::DT; ++dt)
+      v[dt] = r0 * L::VRB + 64 * (dt ^ L::vswz(r0)) + 32 * (grp & 1) + 8 * (c16 & 3);
   }
 };
 
@@ -314,9 +331,11 @@ __device__ __forceinline__ void m_kread(uint32_t ka, bf16x8 &r) {   // k-step IT
                : "v"(ka), "i"((IT >> 1) * 32 + (IT & 1) * 32 * L::KRB));
 }
 template <int D, int IT>
-__device__ __forceinline__ void m_vread(uint32_t va, bf16x8 &r) {   // k-step IT/DT, d-block IT%DT
+__device__ __forceinline__ void m_vread(const uint32_t (&vas)[AttnLayout<D>::DT],
+                                        bf16x8 &r) {   // k-step IT/DT, d-block IT%DT
   using L = AttnLayout<D>;
-  constexpr int off = (IT % L::DT) * 64 + (IT / L::DT) * 16 * L::VRB;
+  const uint32_t va = vas[IT % L::DT];
+  constexpr int off = (IT / L::DT) * 16 * L::VRB;
   uint2 lo, hi;
   asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(lo) : "v"(va), "i"(off));
   asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(hi) : "v"(va), "i"(off + 8 * L::VRB));
@@ -341,7 +360,10 @@ __device__ __forceinline__ void m_tile(uint32_t kt, uint32_t vt, const TileOffse
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[kb][e] = 0.f;
   }
-  const uint32_t ka = kt + to.k, va = vt + to.v;
+  const uint32_t ka = kt + to.k;
+  uint32_t va[L::DT];
+#pragma unroll
+  for (int dt = 0; dt < L::DT; ++dt) va[dt] = vt + to.v[dt];
   // The counts below assume only these reads are outstanding on the LGKM
   // counter (scalar loads return out of order): drain it first.
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -589,8 +611,9 @@ __device__ __forceinline__ void attn_finish(const AttnState<D> &st, const QRow<D
     lse[(size_t)qr.t * Hq + qr.head] = l > 0.f ? (st.m + log2f(l)) * kLn2 : -INFINITY;
   if (!o) return;
   // slice row stride: 16 rows of a 64-lane write land on distinct bank pairs
-  constexpr int OS = L::RB + 16;
-  static_assert(kAttnQPW * OS * attn_max_waves<D>() <= L::bytes(true), "slices fit the tiles");
+  constexpr int OS = L::FINISH_OS;
+  static_assert(kAttnQPW * OS * attn_max_waves<D>() <= L::lds_bytes(true, attn_max_waves<D>()),
+                "slices fit the tile storage");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   char *slice = lds + wave * kAttnQPW * OS;
   const float inv = l > 0.f ? 1.f / l : 0.f;

@@ -40,7 +40,7 @@ __global__ __launch_bounds__(attn_max_waves<D>() * 64) SP_ATTN_OCCUPANCY(D) void
     const uint16_t *__restrict__ v, uint16_t *__restrict__ o, float *__restrict__ lse) {
   using L = AttnLayout<D>;
   constexpr int kNW = attn_max_waves<D>();
-  __shared__ __align__(16) char lds[L::bytes(WANT_O)];
+  __shared__ __align__(16) char lds[L::lds_bytes(WANT_O, kNW)];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int h = lane >> 5, n = lane & 31;

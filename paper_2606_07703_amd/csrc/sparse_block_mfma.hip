@@ -60,7 +60,7 @@ __global__ __launch_bounds__(NW * 64) SP_ATTN_OCCUPANCY(D) void sparse_block_ker
   using L = AttnLayout<D>;
   constexpr int NT = NW * 64;
   constexpr int kMaxSupport = max_support(D, PAGED);
-  __shared__ __align__(16) char lds[L::bytes(true)];
+  __shared__ __align__(16) char lds[L::lds_bytes(true, NW)];
   __shared__ int red_cnt[2][NW];
   __shared__ __align__(16) int ir[kMaxSupport];
   // paged cache: the K/V row of each support entry (ir keeps the position)
