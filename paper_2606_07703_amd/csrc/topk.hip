@@ -17,8 +17,9 @@
 // topk_reg_kernel keeps the row in registers (each thread owns runs of 16
 // consecutive positions) for rows of up to 32768 candidates; the exact zero
 // keys that ReLU produces in bulk are counted by wave ballots instead of
-// contended LDS atomics. topk_rows_kernel streams longer rows from memory on
-// every pass.
+// contended LDS atomics, and when few keys share the threshold's top 22 bits
+// they are ranked directly instead of by the third pass. topk_rows_kernel
+// streams longer rows from memory on every pass, 512 threads a row.
 #include "common.hpp"
 #include "kernels.hpp"
 
