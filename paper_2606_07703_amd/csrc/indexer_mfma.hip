@@ -15,8 +15,10 @@
 //   reduces over the b queries of each selection block (max or sum) before
 //   anything leaves the chip; one float per (block, key) is stored.
 // * indexer_rows_kernel (b = 1): every causal score is stored. The MFMA is
-//   issued with keys as rows (scores transposed) so that each lane holds
-//   four consecutive keys of one query and writes them as one 16-byte store.
+//   issued with keys as rows (scores transposed), so a lane holds runs of
+//   four consecutive keys of one query; each wave passes a tile's scores
+//   through a few LDS rows so that a store instruction writes whole row
+//   segments of 4 (or 8) queries instead of 64 bytes of 16 queries.
 #include <math.h>
 
 #include <atomic>
@@ -530,10 +532,16 @@ __global__ __launch_bounds__(256) void indexer_rows_kernel(int S, int qo, int re
   constexpr int NT = 256, NW = 4;
   constexpr int KT = Tile<DI>::KT, RB = Tile<DI>::RB, KS = Tile<DI>::KS;
   constexpr int QG = NW * kQW;
+  constexpr int KR = KT / 16;          // 16-key row tiles of a key tile
+  constexpr int SRB = KT * 4 + 16;     // staging row stride: 16 rows of a 16-byte write on distinct banks
+  constexpr int LPR = KT * 4 / 16;     // lanes per staged row
+  constexpr int RPI = 64 / LPR;        // rows per store instruction
   __shared__ __align__(16) char lds[2][Tile<DI>::BYTES];
+  __shared__ __align__(16) char stage_rows[NW][16 * SRB];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, c16 = lane & 15;
+  char *stg = stage_rows[wave];
   const int q0 = qo + blockIdx.x * QG;   // qi and Z are addressed by position
   const int k_begin = blockIdx.y * kKC;
   const int q_last = min(q0 + QG, S) - 1;
@@ -564,42 +572,70 @@ __global__ __launch_bounds__(256) void indexer_rows_kernel(int S, int qo, int re
     if (more) stage.load(ki, S, kt0 + KT, tid);
     const char *cur = lds[it & 1];
     if (kt0 <= qw_last) {
+      // One 16-query piece at a time (K fragments are re-read from LDS per
+      // piece; this kernel is bound by its stores): acc[kr] holds keys
+      // kt0 + 16kr + 4g .. +3 of query qw0 + 16qc + c16. The scaled scores
+      // go to the wave's staging rows (row c16, keys 16kr + 4g .. +3), are
+      // read back one row segment per LPR lanes and stored as whole rows of
+      // the tile: RPI query rows of KT consecutive keys per instruction,
+      // where a store straight from the MFMA layout would touch 16 rows.
 #pragma unroll
-      for (int kr = 0; kr < KT / 16; ++kr) {
-        f32x4 acc[4];
+      for (int qc = 0; qc < 4; ++qc) {
+        const int tq0 = qw0 + qc * 16;
+        if (tq0 > qw_last || kt0 > tq0 + 15) continue;   // no causal pair (wave-uniform)
+        f32x4 acc[KR];
 #pragma unroll
-        for (int qc = 0; qc < 4; ++qc) acc[qc] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int kr = 0; kr < KR; ++kr) {
+          acc[kr] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 a = as_bf16x8(lds16(cur + (kr * 16 + c16) * RB + ks * 64 + g * 16));
-#pragma unroll
-          for (int qc = 0; qc < 4; ++qc) acc[qc] = mfma16(a, bq[qc][ks], acc[qc]);
+          for (int ks = 0; ks < KS; ++ks)
+            acc[kr] = mfma16(as_bf16x8(lds16(cur + (kr * 16 + c16) * RB + ks * 64 + g * 16)),
+                             bq[qc][ks], acc[kr]);
         }
-        const int s0 = kt0 + kr * 16 + g * 4;  // this lane's four consecutive keys
 #pragma unroll
-        for (int qc = 0; qc < 4; ++qc) {
-          const int t = qw0 + qc * 16 + c16;
-          if (t > qw_last || s0 > t) continue;
-          float x[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            x[r] = acc[qc][r] * scale;
-            if (relu) x[r] = x[r] > 0.f ? x[r] : 0.f;
+        for (int kr = 0; kr < KR; ++kr) {
+          float4 x;
+          x.x = acc[kr][0] * scale;
+          x.y = acc[kr][1] * scale;
+          x.z = acc[kr][2] * scale;
+          x.w = acc[kr][3] * scale;
+          if (relu) {
+            x.x = x.x > 0.f ? x.x : 0.f;
+            x.y = x.y > 0.f ? x.y : 0.f;
+            x.z = x.z > 0.f ? x.z : 0.f;
+            x.w = x.w > 0.f ? x.w : 0.f;
           }
+          *reinterpret_cast<float4 *>(stg + c16 * SRB + kr * 64 + g * 16) = x;
+        }
+        // the reads below take other lanes' rows
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int j = 0; j < 16 / RPI; ++j) {
+          const int rr = j * RPI + lane / LPR, cc = lane % LPR;
+          const float4 x = *reinterpret_cast<const float4 *>(stg + rr * SRB + cc * 16);
+          const int t = tq0 + rr, s0 = kt0 + cc * 4;
           float *dst = Z + (size_t)t * S + s0;
+          if (t > qw_last || s0 > t) continue;
           if (s0 + 3 <= t) {
             if constexpr (VEC) {
-              *reinterpret_cast<float4 *>(dst) = make_float4(x[0], x[1], x[2], x[3]);
+              *reinterpret_cast<float4 *>(dst) = x;
             } else {
-#pragma unroll
-              for (int r = 0; r < 4; ++r) dst[r] = x[r];
+              dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
             }
           } else {
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (s0 + r <= t) dst[r] = x[r];
+            // the diagonal: a loop, so that its first store is not merged
+            // with the 16-byte store above (which would split that store)
+#pragma unroll 1
+            for (int r = 0; s0 + r <= t; ++r)
+              dst[r] = r == 0 ? x.x : (r == 1 ? x.y : x.z);
           }
         }
+        // the next piece's writes reuse the rows just read
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       }
     }
     if (more) stage.store(lds[(it + 1) & 1], tid);

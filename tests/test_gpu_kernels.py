@@ -302,6 +302,8 @@ INDEXER_CASES = [
     (300, 256, 64, "max", 0, "bf16"),
     (300, 64, 7, "sum", 0, "f32"),
     (1000, 128, 128, "max", 1, "bf16"),
+    (333, 256, 1, "max", 1, "bf16"),    # per query, 32-key tiles: 8 rows per store, rows unaligned
+    (2050, 64, 1, "max", 0, "bf16"),    # per query, three key chunks, ragged last tile
 ]
 
 
