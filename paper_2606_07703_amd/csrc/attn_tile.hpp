@@ -599,8 +599,9 @@ struct AttnPipe {
 // buffers (idle once every wave has left the pipeline), reads them back
 // row-major and stores whole rows: 1 KiB of consecutive rows per
 // instruction. A row's destination comes from the lane that owns it by a
-// lane shuffle. Every wave of the workgroup calls this (it starts with a
-// workgroup barrier); lds is the pipeline's tile storage.
+// lane shuffle. Every wave of the workgroup calls this (when o is given, it
+// waits at a workgroup barrier before touching the tiles); lds is the
+// pipeline's tile storage.
 template <int D>
 __device__ __forceinline__ void attn_finish(const AttnState<D> &st, const QRow<D> &qr, int Hq,
                                             uint16_t *__restrict__ o, float *__restrict__ lse,
