@@ -70,18 +70,18 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 
 template <int D>
 struct AttnLayout {
-  // K and V tiles (64 rows of D bf16) are row-major. K rows are padded: row
-  // stride KRB puts the 16 rows of a b128 operand-read phase on distinct
-  // banks. V rows are not padded; instead the 64-byte groups of row r are
-  // permuted, group g stored at g ^ vswz(r), so the 4 rows a transpose-read
-  // phase touches land on 4 different 16-bank groups. The permutation
-  // depends only on r mod 4 (r mod 4 / 2 at D = 64), so every K read, and
-  // every V read of one 32-dim block, is one lane base plus an immediate
-  // offset. A tile is a whole number of 1 KiB chunks (the unit of a
-  // direct-to-LDS load).
+  // K and V tiles (64 rows of D bf16) are row-major with unpadded rows, and
+  // the pieces of each row are permuted by row so that operand reads hit
+  // distinct banks: 16-byte slot c of K row r is stored at c ^ kswz(r) (the
+  // 16 rows of a b128 read phase, same slot, then fall on 16 different
+  // slots), and 64-byte group g of V row r at g ^ vswz(r) (the 4 rows a
+  // transpose-read phase touches fall on 4 different 16-bank groups). Both
+  // depend only on r mod 16, so a K read is one base per k-step, and a V read
+  // one base per 32-dim block, plus an immediate offset. A tile is a whole
+  // number of 1 KiB chunks (the unit of a direct-to-LDS load).
   static constexpr int RB = D * 2;            // bytes of one row in HBM
   static constexpr int C = D / 8;             // 16-byte columns of a row
-  static constexpr int KSLOTS = C + 1;        // 16-byte slots of a K row
+  static constexpr int KSLOTS = C;            // 16-byte slots of a K row
   static constexpr int VSLOTS = C;            // 16-byte slots of a V row
   static constexpr int KRB = 16 * KSLOTS;
   static constexpr int VRB = 16 * VSLOTS;
@@ -91,6 +91,9 @@ struct AttnLayout {
   static constexpr int KS = D / 16;   // k-steps of K Q^T
   static constexpr int DT = D / 32;   // 32-row blocks of O^T (64-byte groups of a V row)
   __host__ __device__ static constexpr int vswz(int r) { return DT >= 4 ? (r & 3) : ((r >> 1) & 1); }
+  // K: 16-byte slot c of row r stored at c ^ kswz(r), so the 16 rows of a
+  // b128 operand-read phase (same slot) land on distinct banks
+  __host__ __device__ static constexpr int kswz(int r) { return D == 64 ? ((r >> 1) & 7) : (r & 15); }
   // two K buffers, then (when the output is wanted) two V buffers
   static constexpr int bytes(bool want_v) { return 2 * KTILE + (want_v ? 2 * VTILE : 0); }
   // the output staging of attn_finish reuses the tiles: 32 rows per wave at
@@ -144,9 +147,9 @@ __device__ __forceinline__ int4 lds_read_i32x4(uint32_t a) {
 // register round trip: a load instruction fills one 1 KiB chunk of the tile
 // (buffer_load_dwordx4 ... lds puts lane L's 16 bytes at byte 16L of it).
 // Lane L of chunk q holds 16-byte slot 64q + L of the tile, that is row
-// (64q + L) / SLOTS, stored column (64q + L) % SLOTS. K: lanes on padding
-// slots load nothing. V: the lane fetches the column whose permuted place
-// that slot is. The chunks of a tile go to the waves in turn.
+// (64q + L) / SLOTS, stored column (64q + L) % SLOTS, and fetches the column
+// whose permuted place that slot is. The chunks of a tile go to the waves in
+// turn.
 template <int D, int NW, bool IS_V>
 struct TileLoader {
   using L = AttnLayout<D>;
@@ -169,9 +172,8 @@ struct TileLoader {
     }
   }
 
-  // Rows outside [0, nrows) read row 0; their keys are masked. Lanes on
-  // padding slots load the row's first 16 bytes into their padding slot,
-  // which nothing reads: no lane of a chunk is masked. Rows are fetched
+  // Rows outside [0, nrows) read row 0; their keys are masked. No lane of a
+  // chunk is masked (the rows have no padding slots). Rows are fetched
   // through a buffer resource (base and size in SGPRs, 32-bit byte offsets
   // per lane); the API keeps k and v below 4 GiB.
   __device__ __forceinline__ static void issue(uint32_t tile, const uint16_t *base, int nrows,
@@ -186,6 +188,7 @@ struct TileLoader {
       const int slot = (q < CHUNKS ? q : 0) * 64 + lane;
       int c = slot % SLOTS;
       if constexpr (IS_V) c ^= 4 * L::vswz(slot / SLOTS);
+      else c ^= L::kswz(slot / SLOTS);
       const uint32_t s = (rw[p] >= 0 && rw[p] < nrows) ? (uint32_t)rw[p] : 0u;
       const uint32_t off = s * row_bytes + (uint32_t)(j * L::RB + (c < L::C ? c : 0) * 16);
       if (CHUNKS % NW == 0 || q < CHUNKS)
@@ -246,18 +249,20 @@ struct AttnState {
 };
 
 // This lane's read offsets into a K tile and a V tile. K fragment (kb, ks)
-// of lane (n, h) is row 32kb + n, bytes 32ks + 16h. V^T fragment (f, dt) of
+// of lane (n, h) is row 32kb + n, slot 2ks + h, stored at (2ks + h) ^
+// kswz(n): one base per k-step. V^T fragment (f, dt) of
 // lane (grp, c16) reads, by transpose, rows 16f + 4h + c16/4 (then +8),
 // d = 32dt + 16(grp%2) + 4(c16%4) onwards, whose 64-byte group dt is stored
 // at dt ^ vswz(row): one base per d-block dt (the same for all the rows this
-// lane reads). The parts that depend on kb, ks and f are immediate offsets.
+// lane reads). The parts that depend on kb and f are immediate offsets.
 template <int D>
 struct TileOffsets {
   using L = AttnLayout<D>;
-  uint32_t k, v[L::DT];
+  uint32_t k[L::KS], v[L::DT];
   __device__ __forceinline__ void init(int lane) {
     const int n = lane & 31, h = lane >> 5, c16 = lane & 15, grp = lane >> 4;
-    k = n * L::KRB + h * 16;
+#pragma unroll
+    for (int ks = 0; ks < L::KS; ++ks) k[ks] = n * L::KRB + ((2 * ks + h) ^ L::kswz(n)) * 16;
     const int r0 = 4 * h + (c16 >> 2);
 #pragma unroll
     for (int dt = 0; dt < L::DT; ++dt)
@@ -324,11 +329,12 @@ __device__ __forceinline__ void exp_tile(const f32x16 (&s)[2], float scale_log2,
 // the tiles the direct-to-LDS loads are filling, and would otherwise wait for
 // every outstanding load before the first read.
 template <int D, int IT>
-__device__ __forceinline__ void m_kread(uint32_t ka, bf16x8 &r) {   // k-step IT/2, key half IT%2
+__device__ __forceinline__ void m_kread(const uint32_t (&kas)[AttnLayout<D>::KS],
+                                        bf16x8 &r) {   // k-step IT/2, key half IT%2
   using L = AttnLayout<D>;
   asm volatile("ds_read_b128 %0, %1 offset:%2"
                : "=v"(r)
-               : "v"(ka), "i"((IT >> 1) * 32 + (IT & 1) * 32 * L::KRB));
+               : "v"(kas[IT >> 1]), "i"((IT & 1) * 32 * L::KRB));
 }
 template <int D, int IT>
 __device__ __forceinline__ void m_vread(const uint32_t (&vas)[AttnLayout<D>::DT],
@@ -360,8 +366,9 @@ __device__ __forceinline__ void m_tile(uint32_t kt, uint32_t vt, const TileOffse
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[kb][e] = 0.f;
   }
-  const uint32_t ka = kt + to.k;
-  uint32_t va[L::DT];
+  uint32_t ka[L::KS], va[L::DT];
+#pragma unroll
+  for (int ks = 0; ks < L::KS; ++ks) ka[ks] = kt + to.k[ks];
 #pragma unroll
   for (int dt = 0; dt < L::DT; ++dt) va[dt] = vt + to.v[dt];
   // The counts below assume only these reads are outstanding on the LGKM
